@@ -1,0 +1,213 @@
+/*
+ * recycle_stage.h — C ABI of one pipeline stage's training step with the
+ * backward pass decoupled into an input-gradient pass and a deferred
+ * weight-gradient pass, after ReCycle (Gandhi et al., SOSP'24).
+ *
+ * The stage is L pre-LN GPT transformer layers (the paper's evaluation trains
+ * Megatron GPT-3 with tensor parallelism 1, Evaluation section, Workloads).
+ * The four compute calls follow the paper's statement of the problem:
+ *
+ *   rc_stage_forward          F of micro-batch (j, k)
+ *   rc_stage_backward_input   B_input: gradient w.r.t. the stage input only,
+ *                             ready to send upstream at once (Decoupled
+ *                             BackProp, section 3.2)
+ *   rc_stage_backward_weight  B_weight: gradients w.r.t. the parameters,
+ *                             deferred, any order, accumulated over own and
+ *                             re-routed micro-batches (sections 3.1, 3.2; the
+ *                             WeightGradStore / WeightBackwardPass of section 5)
+ *   rc_stage_optimizer_step   this stage's AdamW step, issued on its own with
+ *                             no cross-stage synchronisation (Staggered
+ *                             Optimizer, section 3.3; AdamW, section 5)
+ *
+ * Micro-batches are identified as in the op 5-tuple (i, j, k, c, k_s) of the
+ * schedule MILP notation (section 4.2.2): the handle is stage i on pipeline
+ * k_s; each call names (j, k); c is the call itself.
+ *
+ * Conventions for every function:
+ *  - Returns rc_status; RC_OK == 0.  On failure a message is available from
+ *    rc_last_error() (thread-local, valid until the next failing call on
+ *    that thread).
+ *  - Compute calls are asynchronous with respect to the device: they enqueue
+ *    kernels on the handle's HIP stream and return.  Device faults surface as
+ *    RC_ERR_HIP at a later call or at rc_stage_synchronize.
+ *  - A call that returns an error other than RC_ERR_HIP has enqueued no
+ *    device work and left the handle's state unchanged.
+ *  - All device memory is supplied by the caller (three arenas sized by
+ *    rc_stage_memory_requirements); the library allocates none.
+ *  - Several handles per process are allowed (data-parallel peers or
+ *    neighbouring stages emulated on one GPU).  A handle must not be used
+ *    from two threads at once.
+ */
+#ifndef RECYCLE_STAGE_H
+#define RECYCLE_STAGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum rc_status {
+  RC_OK = 0,
+  RC_ERR_INVALID_ARG = -1,   /* null pointer, bad size, unknown id, misaligned buffer */
+  RC_ERR_BAD_STATE = -2,     /* call out of order for this micro-batch / iteration */
+  RC_ERR_OUT_OF_STASH = -3,  /* no free stash slot for another forward */
+  RC_ERR_HIP = -4,           /* a HIP runtime call or kernel launch failed */
+  RC_ERR_UNSUPPORTED = -5    /* shape or option this build does not implement */
+} rc_status;
+
+typedef enum rc_dtype {
+  RC_FP32 = 0,  /* fp32 storage and arithmetic throughout */
+  RC_BF16 = 1   /* bf16 activations / weight copies, fp32 accumulation, fp32 grads, master weights and Adam moments */
+} rc_dtype;
+
+/* Shape of the stage.  Requirements: hidden % heads == 0; hidden, ffn,
+ * seq_len and head_dim = hidden/heads are multiples of 8 (otherwise
+ * RC_ERR_UNSUPPORTED).  causal = 1 masks keys after the query (GPT). */
+typedef struct rc_stage_config {
+  int32_t num_layers;
+  int32_t hidden;
+  int32_t heads;
+  int32_t ffn;
+  int32_t seq_len;
+  int32_t micro_batch;
+  int32_t causal;
+  int32_t dtype;            /* rc_dtype */
+  float ln_eps;             /* LayerNorm epsilon inside the square root */
+  int32_t max_stashed_mb;   /* micro-batches that may hold weight-pass intermediates (F..W) at once */
+  int32_t max_inflight_mb;  /* micro-batches that may hold forward-only intermediates (F..B) at once; <= max_stashed_mb */
+} rc_stage_config;
+
+/* AdamW (Kingma & Ba bias correction, decoupled weight decay).  Weight decay
+ * applies to the four linear weight matrices of each layer only. */
+typedef struct rc_adam_config {
+  float lr, beta1, beta2, eps, weight_decay;
+} rc_adam_config;
+
+/* Micro-batch identity: j = id within the iteration, k = original
+ * data-parallel pipeline (k != the handle's pipeline_id when re-routed). */
+typedef struct rc_mb {
+  int32_t j;
+  int32_t k;
+} rc_mb;
+
+enum { RC_OP_F = 0, RC_OP_B = 1, RC_OP_W = 2, RC_OP_STEP = 3 };
+
+/* One op-log entry: the op 5-tuple (i=stage, j, k, c=op, k_s) plus the
+ * sequence number and the stage-local iteration.  STEP has j = k = -1. */
+typedef struct rc_op_record {
+  int64_t seq;
+  int32_t op;
+  int32_t j;
+  int32_t k;
+  int32_t k_s;
+  int32_t stage;
+  int32_t reserved;
+  int64_t iter;
+} rc_op_record;
+
+/* What rc_stage_read copies out (all fp32, the parameter's natural shape). */
+enum { RC_READ_PARAM = 0, RC_READ_GRAD = 1, RC_READ_ADAM_M = 2, RC_READ_ADAM_V = 3 };
+
+/* Parameter ids within a layer; linear weights are stored [in, out]
+ * (y = x W) and the fused QKV weight [hidden, 3*hidden] has column blocks
+ * Q | K | V, head n using columns n*head_dim .. (n+1)*head_dim-1 of each. */
+enum {
+  RC_P_LN1_G = 0, RC_P_LN1_B = 1, RC_P_W_QKV = 2, RC_P_B_QKV = 3, RC_P_W_O = 4, RC_P_B_O = 5,
+  RC_P_LN2_G = 6, RC_P_LN2_B = 7, RC_P_W_1 = 8, RC_P_B_1 = 9, RC_P_W_2 = 10, RC_P_B_2 = 11,
+  RC_NUM_PARAMS = 12
+};
+
+typedef struct rc_stage rc_stage; /* opaque, library-owned host object */
+
+/* Bytes of the three caller-allocated device arenas:
+ *  state: fp32 master weights, fp32 gradients, Adam m and v, bf16 weight copies;
+ *  stash: max_stashed_mb weight-pass slots + max_inflight_mb forward-only slots
+ *         (the WeightGradStore of section 5; the memory cost the paper names in
+ *         section 3.2, "the memory challenge");
+ *  work:  per-call scratch reused by every call of the handle.
+ * Each arena must be 256-byte aligned.  Pure host function.
+ * Errors: RC_ERR_INVALID_ARG (null pointers, inconsistent config),
+ *         RC_ERR_UNSUPPORTED (shape outside the requirements above). */
+rc_status rc_stage_memory_requirements(const rc_stage_config* cfg, size_t* state_bytes,
+                                       size_t* stash_bytes, size_t* work_bytes);
+
+/* Create stage i = stage_index of pipeline k_s = pipeline_id.  The arenas are
+ * owned by the caller and must stay valid until rc_stage_destroy; their
+ * contents are managed by the library (gradients, m and v are zeroed here,
+ * parameters start at zero until loaded).  hip_stream is a hipStream_t (NULL =
+ * the null stream); every compute call is enqueued on it.
+ * Dry-run handle: pass state_arena == stash_arena == work_arena == NULL.  It
+ * performs only the bookkeeping (state machine, stash slots, op log), enqueues
+ * nothing and touches no device; it validates op lists on the host.
+ * Errors: RC_ERR_INVALID_ARG, RC_ERR_UNSUPPORTED, RC_ERR_HIP. */
+rc_status rc_stage_create(const rc_stage_config* cfg, const rc_adam_config* adam,
+                          int32_t stage_index, int32_t pipeline_id, void* state_arena,
+                          void* stash_arena, void* work_arena, void* hip_stream, rc_stage** out);
+
+/* Waits for the handle's stream, then frees the host object (not the arenas). */
+rc_status rc_stage_destroy(rc_stage* st);
+
+/* Copy fp32 host values into parameter (layer, param_id); bf16 weight copies
+ * are refreshed (round to nearest even).  Synchronous.  host_src holds the
+ * parameter's element count in its natural row-major shape. */
+rc_status rc_stage_load_param(rc_stage* st, int32_t layer, int32_t param_id, const float* host_src);
+
+/* Copy parameter / gradient / Adam moment (what = RC_READ_*) of (layer,
+ * param_id) to host fp32 memory.  Synchronous (waits for the stream).
+ * Gradients are those of the last weight pass, kept until the first weight
+ * pass of the next iteration. */
+rc_status rc_stage_read(rc_stage* st, int32_t what, int32_t layer, int32_t param_id, float* host_dst);
+
+/* F: y = Stage(x) for micro-batch mb.  x, y: device [micro_batch, seq_len,
+ * hidden] row-major in the config dtype; y must not alias x.  The caller owns
+ * both and may reuse them once the stream reaches this point.  Takes one
+ * stash slot and one forward-only slot.
+ * Errors: RC_ERR_BAD_STATE (mb already ran F this iteration),
+ *         RC_ERR_OUT_OF_STASH, RC_ERR_INVALID_ARG, RC_ERR_HIP. */
+rc_status rc_stage_forward(rc_stage* st, rc_mb mb, const void* x, void* y);
+
+/* B_input: dx = J_x(x)^T dy for micro-batch mb; touches no gradient buffer.
+ * dy is copied into the stash; dx may be sent upstream as soon as the stream
+ * reaches this point.  Frees the micro-batch's forward-only slot.
+ * Errors: RC_ERR_BAD_STATE (mb has not run F, or already ran B),
+ *         RC_ERR_INVALID_ARG, RC_ERR_HIP. */
+rc_status rc_stage_backward_input(rc_stage* st, rc_mb mb, const void* dy, void* dx);
+
+/* B_weight: add mb's parameter gradients (X^T dY per linear, column sums for
+ * biases, sum(dout * xhat) / sum(dout) for LayerNorm) into the fp32 gradient
+ * buffers; the first weight pass of an iteration overwrites them.  Any order
+ * over micro-batches.  Frees the micro-batch's stash slot.
+ * Errors: RC_ERR_BAD_STATE (mb has not run B, or already ran W), RC_ERR_HIP. */
+rc_status rc_stage_backward_weight(rc_stage* st, rc_mb mb);
+
+/* AdamW over every parameter of the stage with g = grad_scale * gradient;
+ * refreshes the bf16 weight copies; closes the iteration (every micro-batch
+ * state is reset, the iteration counter advances).  With no weight pass in
+ * the iteration the gradient is zero.
+ * Errors: RC_ERR_BAD_STATE (a micro-batch of the iteration has not run W),
+ *         RC_ERR_HIP. */
+rc_status rc_stage_optimizer_step(rc_stage* st, float grad_scale);
+
+/* Copy up to cap op-log records into buf (may be NULL when cap == 0); *n
+ * receives the total number of records. */
+rc_status rc_stage_op_log(rc_stage* st, rc_op_record* buf, int32_t cap, int32_t* n);
+
+/* Number of micro-batches currently holding a stash slot / a forward-only slot. */
+rc_status rc_stage_stash_usage(rc_stage* st, int32_t* stashed, int32_t* inflight);
+
+/* Replace the handle's stream (subsequent calls enqueue on it). */
+rc_status rc_stage_set_stream(rc_stage* st, void* hip_stream);
+
+/* Wait for the handle's stream; reports any deferred device error as RC_ERR_HIP. */
+rc_status rc_stage_synchronize(rc_stage* st);
+
+/* Message for the last non-OK status on the calling thread ("" if none). */
+const char* rc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RECYCLE_STAGE_H */

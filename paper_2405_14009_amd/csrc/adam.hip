@@ -1,0 +1,83 @@
+// Fused AdamW over the stage's flat fp32 parameter / gradient / moment
+// buffers (coalesced float4 streams), refreshing the bf16 weight copies in
+// the same pass; plus small fill / cast helpers.
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int NT = 256;
+
+__device__ __forceinline__ float adam_one(float p, float g, float& m, float& v, bool decay,
+                                          float lr, float b1, float b2, float eps, float wd,
+                                          float step_size, float inv_sqrt_bc2, float gs) {
+  g *= gs;
+  m = b1 * m + (1.f - b1) * g;
+  v = b2 * v + (1.f - b2) * g * g;
+  if (decay) p *= (1.f - lr * wd);
+  return p - step_size * m / (sqrtf(v) * inv_sqrt_bc2 + eps);
+}
+
+// n and n_decay are multiples of 4 (parameter tensors are padded to 64).
+__global__ __launch_bounds__(NT) void adamw_k(float4* __restrict__ p, const float4* __restrict__ g,
+                                              float4* __restrict__ m, float4* __restrict__ v,
+                                              bf16* __restrict__ wb, long n4, long nd4, float lr,
+                                              float b1, float b2, float eps, float wd,
+                                              float step_size, float inv_sqrt_bc2, float gs) {
+  for (long i = blockIdx.x * (long)NT + threadIdx.x; i < n4; i += (long)gridDim.x * NT) {
+    float4 pp = p[i], gg = g[i], mm = m[i], vv = v[i];
+    const bool dec = i < nd4;
+    pp.x = adam_one(pp.x, gg.x, mm.x, vv.x, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
+    pp.y = adam_one(pp.y, gg.y, mm.y, vv.y, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
+    pp.z = adam_one(pp.z, gg.z, mm.z, vv.z, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
+    pp.w = adam_one(pp.w, gg.w, mm.w, vv.w, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
+    p[i] = pp;
+    m[i] = mm;
+    v[i] = vv;
+    if (wb != nullptr && dec) {
+      bf16* o = wb + 4 * i;
+      o[0] = (bf16)pp.x;
+      o[1] = (bf16)pp.y;
+      o[2] = (bf16)pp.z;
+      o[3] = (bf16)pp.w;
+    }
+  }
+}
+
+__global__ __launch_bounds__(NT) void cast_k(const float* __restrict__ s, bf16* __restrict__ d, long n) {
+  for (long i = blockIdx.x * (long)NT + threadIdx.x; i < n; i += (long)gridDim.x * NT) d[i] = (bf16)s[i];
+}
+
+__global__ __launch_bounds__(NT) void fill_k(float* __restrict__ d, long n, float v) {
+  for (long i = blockIdx.x * (long)NT + threadIdx.x; i < n; i += (long)gridDim.x * NT) d[i] = v;
+}
+
+int grid_for(long n) {
+  long g = (n + NT - 1) / NT;
+  return (int)(g < 8192 ? (g > 0 ? g : 1) : 8192);
+}
+
+}  // namespace
+
+hipError_t adamw_step(float* p, const float* g, float* m, float* v, void* wb, long n, long n_decay,
+                      float lr, float beta1, float beta2, float eps, float wd, float step_size,
+                      float inv_sqrt_bc2, float grad_scale, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if ((n & 3) || (n_decay & 3)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(adamw_k, dim3(grid_for(n / 4)), dim3(NT), 0, s, (float4*)p, (const float4*)g,
+                     (float4*)m, (float4*)v, (bf16*)wb, n / 4, n_decay / 4, lr, beta1, beta2, eps,
+                     wd, step_size, inv_sqrt_bc2, grad_scale);
+  return hipGetLastError();
+}
+
+hipError_t cast_f32_to_bf16(const float* src, void* dst, long n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(cast_k, dim3(grid_for(n)), dim3(NT), 0, s, src, (bf16*)dst, n);
+  return hipGetLastError();
+}
+
+hipError_t fill_f32(float* dst, long n, float value, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_k, dim3(grid_for(n)), dim3(NT), 0, s, dst, n, value);
+  return hipGetLastError();
+}

@@ -1,0 +1,85 @@
+// GEMM entry points used by the stage runtime, and the shared epilogue.
+//
+// C[m, n] = sum_k A(m, k) B(k, n) with
+//   A(m, k) = a_kcontig ? A[m*lda + k] : A[k*lda + m]
+//   B(k, n) = b_kcontig ? B[n*ldb + k] : B[k*ldb + n]
+// so every operand layout of the stage maps onto one kernel family:
+//   forward  Y  = X W      : A k-contiguous, B n-contiguous (W stored [in, out])
+//   dgrad    dX = dY W^T   : A k-contiguous, B k-contiguous
+//   wgrad    dW = X^T dY   : A m-contiguous, B n-contiguous (reduction over tokens)
+// Optional batching over z = blockIdx.y in [0, batch*heads) adds
+// (z / heads) * *_bs + (z % heads) * *_hs elements to A, B and C (attention).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "common.h"
+
+enum EpiKind {
+  EPI_STORE = 0,       // C = acc                                (activation type)
+  EPI_BIAS = 1,        // C = acc + bias[n]
+  EPI_BIAS_RESID = 2,  // C = acc + bias[n] + resid[m, n]
+  EPI_BIAS_GELU = 3,   // C = U = acc + bias[n];  C2 = gelu(U)
+  EPI_GELU_BWD = 4,    // C = acc * gelu'(aux[m, n])
+  EPI_F32_ACC = 5,     // C32 = (accumulate ? C32 : 0) + acc     (fp32 gradient buffers)
+  EPI_F32_STORE = 6    // C32 = acc                              (fp32 scores)
+};
+
+enum KRange {
+  KR_FULL = 0,   // k in [0, K)
+  KR_BELOW = 1,  // k < min(K, m0 + BM): operand A is zero for k > m (causal P, dS)
+  KR_ABOVE = 2   // k >= m0 rounded down: operand A is zero for k < m (transposed causal P, dS)
+};
+
+struct GemmParams {
+  int M, N, K;
+  const void* A; long lda; int a_kcontig;
+  const void* B; long ldb; int b_kcontig;
+  int batch, heads;
+  long a_bs, a_hs, b_bs, b_hs, c_bs, c_hs;
+  int causal_skip;  // skip output tiles strictly above the diagonal (n0 > m0 + BM - 1)
+  int krange;       // KRange
+  int epi;          // EpiKind
+  void* C; long ldc;
+  const float* bias;
+  const void* resid; long ld_resid;
+  const void* aux; long ld_aux;
+  void* C2; long ldc2;
+  int accumulate;
+};
+
+// Shapes must satisfy: M, N, K multiples of 8 when an operand is loaded
+// along that dimension in 8-element vectors (checked by the caller).
+hipError_t gemm_bf16(const GemmParams& p, hipStream_t s);
+hipError_t gemm_f32(const GemmParams& p, hipStream_t s);
+
+template <int EPI, class E>
+__device__ __forceinline__ void epi_store(const GemmParams& p, E* C, int m, int n, float v) {
+  const long i = (long)m * p.ldc + n;
+  if constexpr (EPI == EPI_STORE) {
+    C[i] = from_f32<E>(v);
+  } else if constexpr (EPI == EPI_BIAS) {
+    C[i] = from_f32<E>(v + p.bias[n]);
+  } else if constexpr (EPI == EPI_BIAS_RESID) {
+    const E* r = (const E*)p.resid;
+    C[i] = from_f32<E>(v + p.bias[n] + to_f32(r[(long)m * p.ld_resid + n]));
+  } else if constexpr (EPI == EPI_BIAS_GELU) {
+    float u = v + p.bias[n];
+    C[i] = from_f32<E>(u);
+    ((E*)p.C2)[(long)m * p.ldc2 + n] = from_f32<E>(gelu_f(u));
+  } else if constexpr (EPI == EPI_GELU_BWD) {
+    const E* u = (const E*)p.aux;
+    C[i] = from_f32<E>(v * gelu_grad_f(to_f32(u[(long)m * p.ld_aux + n])));
+  } else if constexpr (EPI == EPI_F32_ACC) {
+    float* c = (float*)C;
+    c[i] = p.accumulate ? c[i] + v : v;
+  } else {  // EPI_F32_STORE
+    ((float*)C)[i] = v;
+  }
+}
+
+// Output element type of each epilogue given the activation type E.
+template <int EPI, class E>
+struct EpiOut { typedef E type; };
+template <class E> struct EpiOut<EPI_F32_ACC, E> { typedef float type; };
+template <class E> struct EpiOut<EPI_F32_STORE, E> { typedef float type; };

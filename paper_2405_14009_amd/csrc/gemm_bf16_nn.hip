@@ -1,0 +1,24 @@
+// bf16 GEMMs with A k-contiguous and B n-contiguous (forward Y = X W, and
+// the attention products P V and dS K), plus the top-level bf16 dispatcher.
+#include "gemm_bf16_kernel.h"
+
+hipError_t gemm_bf16_nt(const GemmParams& p, hipStream_t s);
+hipError_t gemm_bf16_tn(const GemmParams& p, hipStream_t s);
+
+static hipError_t gemm_bf16_nn(const GemmParams& p, hipStream_t s) {
+  switch (p.epi) {
+    case EPI_STORE: return launch_bf16<true, false, EPI_STORE>(p, s);
+    case EPI_BIAS: return launch_bf16<true, false, EPI_BIAS>(p, s);
+    case EPI_BIAS_RESID: return launch_bf16<true, false, EPI_BIAS_RESID>(p, s);
+    case EPI_BIAS_GELU: return launch_bf16<true, false, EPI_BIAS_GELU>(p, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t gemm_bf16(const GemmParams& p, hipStream_t s) {
+  if (p.M <= 0 || p.N <= 0 || p.batch * p.heads <= 0) return hipSuccess;
+  if (p.a_kcontig && !p.b_kcontig) return gemm_bf16_nn(p, s);
+  if (p.a_kcontig && p.b_kcontig) return gemm_bf16_nt(p, s);
+  if (!p.a_kcontig && !p.b_kcontig) return gemm_bf16_tn(p, s);
+  return hipErrorInvalidValue;
+}

@@ -1,0 +1,45 @@
+// Host-side launchers of the non-GEMM stage kernels.  Every launcher
+// enqueues on the given stream and returns hipGetLastError().
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+// LayerNorm forward over rows of width h: y = (x - mean) * rstd * g + b;
+// mean and rstd (fp32) are saved per row.  elt: 2 = bf16, 4 = fp32.
+hipError_t ln_forward(int elt, const void* x, const float* g, const float* b, void* y, float* mean,
+                      float* rstd, long rows, int h, float eps, hipStream_t s);
+
+// LayerNorm input gradient plus residual: dx = resid + rstd * (dz - mean(dz)
+// - xhat * mean(dz * xhat)), dz = dout * g, xhat recomputed from x, mean, rstd.
+hipError_t ln_backward(int elt, const void* dout, const void* x, const float* mean,
+                       const float* rstd, const float* g, const void* resid, void* dx, long rows,
+                       int h, hipStream_t s);
+
+// Column reductions over rows of a [rows, n] matrix with leading dimension ld,
+// into fp32 outputs (overwrite or accumulate), deterministic two-stage:
+//   bias:  db[c] (+)= sum_r dout[r, c]
+//   ln:    dg[c] (+)= sum_r dout[r, c] * (x[r, c] - mean[r]) * rstd[r];  db as above
+// part must hold 2 * ceil(rows / 64) * n floats.
+hipError_t colsum_bias(int elt, const void* dout, long ld, long rows, int n, float* db,
+                       int accumulate, float* part, hipStream_t s);
+hipError_t colsum_ln(int elt, const void* dout, const void* x, const float* mean,
+                     const float* rstd, long rows, int n, float* dg, float* db, int accumulate,
+                     float* part, hipStream_t s);
+long colsum_part_floats(long rows, int n);
+
+// Attention softmax over materialised scores, rows of length s, z*s rows.
+//   forward:  P[r, c] = exp(scale S[r, c] - max) / sum  for c <= q (causal) else 0
+//   backward: dS[r, c] = scale * P[r, c] * (dP[r, c] - sum_c' dP P)  (0 where masked)
+hipError_t softmax_forward(int elt, const float* S, void* P, long rows, int s, float scale,
+                           int causal, hipStream_t st);
+hipError_t softmax_backward(int elt, const float* dP, const void* P, void* dS, long rows, int s,
+                            float scale, int causal, hipStream_t st);
+
+// AdamW over n fp32 parameters; weight decay on indices < n_decay; when wb is
+// non-null the first n_decay updated values are also written to it in bf16.
+hipError_t adamw_step(float* p, const float* g, float* m, float* v, void* wb, long n, long n_decay,
+                      float lr, float beta1, float beta2, float eps, float wd, float step_size,
+                      float inv_sqrt_bc2, float grad_scale, hipStream_t s);
+
+hipError_t cast_f32_to_bf16(const float* src, void* dst, long n, hipStream_t s);
+hipError_t fill_f32(float* dst, long n, float value, hipStream_t s);

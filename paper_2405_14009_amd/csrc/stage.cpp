@@ -1,0 +1,689 @@
+// Stage runtime behind the C ABI of include/recycle_stage.h.
+//
+// One handle = pipeline stage i on data-parallel pipeline k_s.  It owns no
+// device memory: three caller arenas hold
+//   state: flat fp32 master weights | fp32 gradients | Adam m | Adam v, then
+//          the bf16 copies of the weight matrices (bf16 stages).  Matrices of
+//          all layers come first, so weight decay applies to one prefix.
+//   stash: the WeightGradStore (ReCycle, section 5): max_stashed_mb weight-pass
+//          slots (held from F to W) and max_inflight_mb forward-only slots
+//          (held from F to B), each laid out per layer.
+//   work:  scratch reused by every call (attention scores, dO, reduction partials).
+// Each call checks the micro-batch state machine on the host first, then
+// enqueues its kernel sequence on the handle's stream and returns.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <array>
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "gemm.h"
+#include "kernels.h"
+#include "recycle_stage.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+rc_status fail(rc_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+#define HIPCHK(expr)                                                                     \
+  do {                                                                                   \
+    hipError_t e_ = (expr);                                                              \
+    if (e_ != hipSuccess)                                                                \
+      return fail(RC_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(e_));        \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+long pad64(long n) { return (n + 63) / 64 * 64; }
+
+const int kMatrixIds[4] = {RC_P_W_QKV, RC_P_W_O, RC_P_W_1, RC_P_W_2};
+const int kVectorIds[8] = {RC_P_LN1_G, RC_P_LN1_B, RC_P_B_QKV, RC_P_B_O,
+                           RC_P_LN2_G, RC_P_LN2_B, RC_P_B_1, RC_P_B_2};
+
+struct PLoc {
+  long off = 0, count = 0;
+};
+
+// Byte offsets inside one layer of a weight-pass slot.
+struct WLayer {
+  size_t X, A, O, H, C, G, dY, dQKV, dH, dU, dA, dC, mu1, r1, mu2, r2, bytes;
+};
+// Byte offsets inside one layer of a forward-only slot.
+struct FLayer {
+  size_t QKV, U, P, bytes;
+};
+
+struct Layout {
+  int L, h, a, d, f, s, b, elt, causal;
+  long T;
+  bool bf;
+  float eps;
+  int wslots, fslots;
+  std::vector<std::array<PLoc, RC_NUM_PARAMS>> p;
+  long n_mat, n_total;
+  size_t off_master, off_grad, off_m, off_v, off_wb, state_bytes;
+  WLayer w;
+  FLayer fl;
+  size_t wslot_bytes, fslot_bytes, off_fslots, stash_bytes;
+  size_t off_S, off_dS, off_dO, off_part, work_bytes;
+};
+
+rc_status make_layout(const rc_stage_config* c, Layout& y) {
+  if (!c) return fail(RC_ERR_INVALID_ARG, "null config");
+  if (c->num_layers < 1 || c->hidden < 1 || c->heads < 1 || c->ffn < 1 || c->seq_len < 1 ||
+      c->micro_batch < 1)
+    return fail(RC_ERR_INVALID_ARG, "config sizes must be positive");
+  if (c->dtype != RC_FP32 && c->dtype != RC_BF16) return fail(RC_ERR_INVALID_ARG, "unknown dtype");
+  if (c->causal != 0 && c->causal != 1) return fail(RC_ERR_INVALID_ARG, "causal must be 0 or 1");
+  if (c->max_stashed_mb < 1 || c->max_inflight_mb < 1 || c->max_inflight_mb > c->max_stashed_mb)
+    return fail(RC_ERR_INVALID_ARG, "need 1 <= max_inflight_mb <= max_stashed_mb");
+  if (!(c->ln_eps >= 0.f)) return fail(RC_ERR_INVALID_ARG, "ln_eps must be >= 0");
+  if (c->hidden % c->heads) return fail(RC_ERR_UNSUPPORTED, "hidden must be a multiple of heads");
+  const int d = c->hidden / c->heads;
+  if (c->hidden % 8 || c->ffn % 8 || c->seq_len % 8 || d % 8)
+    return fail(RC_ERR_UNSUPPORTED, "hidden, ffn, seq_len and head_dim must be multiples of 8");
+  y.L = c->num_layers;
+  y.h = c->hidden;
+  y.a = c->heads;
+  y.d = d;
+  y.f = c->ffn;
+  y.s = c->seq_len;
+  y.b = c->micro_batch;
+  y.T = (long)c->micro_batch * c->seq_len;
+  y.bf = c->dtype == RC_BF16;
+  y.elt = y.bf ? 2 : 4;
+  y.causal = c->causal;
+  y.eps = c->ln_eps;
+  y.wslots = c->max_stashed_mb;
+  y.fslots = c->max_inflight_mb;
+  const long h = y.h, f = y.f;
+  const long msize[RC_NUM_PARAMS] = {h, h, h * 3 * h, 3 * h, h * h, h, h, h, h * f, f, f * h, h};
+  y.p.assign(y.L, {});
+  long off = 0;
+  for (int l = 0; l < y.L; ++l)
+    for (int pid : kMatrixIds) {
+      y.p[l][pid] = {off, msize[pid]};
+      off += pad64(msize[pid]);
+    }
+  y.n_mat = off;
+  for (int l = 0; l < y.L; ++l)
+    for (int pid : kVectorIds) {
+      y.p[l][pid] = {off, msize[pid]};
+      off += pad64(msize[pid]);
+    }
+  y.n_total = off;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t r = o;
+    o = align_up(o + bytes);
+    return r;
+  };
+  y.off_master = take(4 * y.n_total);
+  y.off_grad = take(4 * y.n_total);
+  y.off_m = take(4 * y.n_total);
+  y.off_v = take(4 * y.n_total);
+  y.off_wb = take(y.bf ? 2 * y.n_mat : 0);
+  y.state_bytes = o;
+
+  const size_t E = y.elt, T = y.T;
+  o = 0;
+  WLayer& w = y.w;
+  w.X = take(T * h * E);
+  w.A = take(T * h * E);
+  w.O = take(T * h * E);
+  w.H = take(T * h * E);
+  w.C = take(T * h * E);
+  w.G = take(T * f * E);
+  w.dY = take(T * h * E);
+  w.dQKV = take(T * 3 * h * E);
+  w.dH = take(T * h * E);
+  w.dU = take(T * f * E);
+  w.dA = take(T * h * E);
+  w.dC = take(T * h * E);
+  w.mu1 = take(T * 4);
+  w.r1 = take(T * 4);
+  w.mu2 = take(T * 4);
+  w.r2 = take(T * 4);
+  w.bytes = o;
+  o = 0;
+  const size_t ss = (size_t)y.b * y.a * y.s * y.s;
+  y.fl.QKV = take(T * 3 * h * E);
+  y.fl.U = take(T * f * E);
+  y.fl.P = take(ss * E);
+  y.fl.bytes = o;
+  y.wslot_bytes = (size_t)y.L * w.bytes;
+  y.fslot_bytes = (size_t)y.L * y.fl.bytes;
+  y.off_fslots = (size_t)y.wslots * y.wslot_bytes;
+  y.stash_bytes = y.off_fslots + (size_t)y.fslots * y.fslot_bytes;
+  o = 0;
+  y.off_S = take(ss * 4);
+  y.off_dS = take(ss * E);
+  y.off_dO = take(T * h * E);
+  y.off_part = take(4 * colsum_part_floats(y.T, (int)std::max(3 * h, f)));
+  y.work_bytes = o;
+  return RC_OK;
+}
+
+struct MbRec {
+  int state;  // 1 = F done, 2 = B done, 3 = W done
+  int ws, fs;
+};
+
+}  // namespace
+
+struct rc_stage {
+  rc_stage_config cfg;
+  rc_adam_config adam;
+  int stage_index, pipeline_id;
+  bool dry;
+  hipStream_t stream;
+  char *state, *stash, *work;
+  Layout lay;
+  std::map<std::pair<int, int>, MbRec> mbs;
+  std::vector<int> free_w, free_f;
+  std::vector<rc_op_record> log;
+  int64_t iter = 0, t = 0;
+  bool grads_fresh = true;
+};
+
+namespace {
+
+struct WPtr {
+  char *X, *A, *O, *H, *C, *G, *dY, *dQKV, *dH, *dU, *dA, *dC;
+  float *mu1, *r1, *mu2, *r2;
+};
+struct FPtr {
+  char *QKV, *U, *P;
+};
+
+WPtr wptr(rc_stage* st, int slot, int l) {
+  const Layout& y = st->lay;
+  char* b = st->stash + (size_t)slot * y.wslot_bytes + (size_t)l * y.w.bytes;
+  const WLayer& w = y.w;
+  return {b + w.X, b + w.A, b + w.O, b + w.H, b + w.C, b + w.G, b + w.dY, b + w.dQKV,
+          b + w.dH, b + w.dU, b + w.dA, b + w.dC, (float*)(b + w.mu1), (float*)(b + w.r1),
+          (float*)(b + w.mu2), (float*)(b + w.r2)};
+}
+
+FPtr fptr(rc_stage* st, int slot, int l) {
+  const Layout& y = st->lay;
+  char* b = st->stash + y.off_fslots + (size_t)slot * y.fslot_bytes + (size_t)l * y.fl.bytes;
+  return {b + y.fl.QKV, b + y.fl.U, b + y.fl.P};
+}
+
+float* master(rc_stage* st, int l, int pid) {
+  return (float*)(st->state + st->lay.off_master) + st->lay.p[l][pid].off;
+}
+float* gradp(rc_stage* st, int l, int pid) {
+  return (float*)(st->state + st->lay.off_grad) + st->lay.p[l][pid].off;
+}
+// Weight matrix as read by the GEMMs: the bf16 copy for bf16 stages.
+const void* weight(rc_stage* st, int l, int pid) {
+  if (st->lay.bf) return (const char*)(st->state + st->lay.off_wb) + 2 * st->lay.p[l][pid].off;
+  return master(st, l, pid);
+}
+
+// Element offset into an activation buffer.
+inline char* el(void* p, long n, int elt) { return (char*)p + n * elt; }
+
+GemmParams gp(int M, int N, int K, const void* A, long lda, int ak, const void* B, long ldb, int bk,
+              int epi, void* C, long ldc) {
+  GemmParams g;
+  std::memset(&g, 0, sizeof(g));
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.A = A;
+  g.lda = lda;
+  g.a_kcontig = ak;
+  g.B = B;
+  g.ldb = ldb;
+  g.b_kcontig = bk;
+  g.batch = 1;
+  g.heads = 1;
+  g.epi = epi;
+  g.C = C;
+  g.ldc = ldc;
+  return g;
+}
+
+hipError_t gemm(rc_stage* st, const GemmParams& g) {
+  return st->lay.bf ? gemm_bf16(g, st->stream) : gemm_f32(g, st->stream);
+}
+
+// Per (sequence, head) batching of the attention products; Q, K, V and dQ,
+// dK, dV live as column blocks of the [T, 3h] QKV / dQKV matrices and O, dO
+// as head columns of [T, h] matrices.
+void batch_heads(GemmParams& g, const Layout& y, long a_bs, long a_hs, long b_bs, long b_hs,
+                 long c_bs, long c_hs) {
+  g.batch = y.b;
+  g.heads = y.a;
+  g.a_bs = a_bs;
+  g.a_hs = a_hs;
+  g.b_bs = b_bs;
+  g.b_hs = b_hs;
+  g.c_bs = c_bs;
+  g.c_hs = c_hs;
+}
+
+rc_status attn_forward(rc_stage* st, char* QKV, char* P, char* O) {
+  const Layout& y = st->lay;
+  const int E = y.elt;
+  const long s = y.s, h = y.h, d = y.d, ss = s * s;
+  float* S = (float*)(st->work + y.off_S);
+  GemmParams g = gp(y.s, y.s, y.d, QKV, 3 * h, 1, el(QKV, h, E), 3 * h, 1, EPI_F32_STORE, S, s);
+  batch_heads(g, y, s * 3 * h, d, s * 3 * h, d, y.a * ss, ss);
+  g.causal_skip = y.causal;
+  HIPCHK(gemm(st, g));
+  HIPCHK(softmax_forward(E, S, P, (long)y.b * y.a * y.s, y.s, 1.0f / std::sqrt((float)y.d),
+                         y.causal, st->stream));
+  g = gp(y.s, y.d, y.s, P, s, 1, el(QKV, 2 * h, E), 3 * h, 0, EPI_STORE, O, h);
+  batch_heads(g, y, y.a * ss, ss, s * 3 * h, d, s * h, d);
+  g.krange = y.causal ? KR_BELOW : KR_FULL;
+  HIPCHK(gemm(st, g));
+  return RC_OK;
+}
+
+rc_status attn_backward(rc_stage* st, char* QKV, char* P, char* dO, char* dQKV) {
+  const Layout& y = st->lay;
+  const int E = y.elt;
+  const long s = y.s, h = y.h, d = y.d, ss = s * s;
+  float* dP = (float*)(st->work + y.off_S);
+  char* dS = st->work + y.off_dS;
+  GemmParams g = gp(y.s, y.s, y.d, dO, h, 1, el(QKV, 2 * h, E), 3 * h, 1, EPI_F32_STORE, dP, s);
+  batch_heads(g, y, s * h, d, s * 3 * h, d, y.a * ss, ss);
+  g.causal_skip = y.causal;
+  HIPCHK(gemm(st, g));
+  HIPCHK(softmax_backward(E, dP, P, dS, (long)y.b * y.a * y.s, y.s, 1.0f / std::sqrt((float)y.d),
+                          y.causal, st->stream));
+  // dQ = dS K
+  g = gp(y.s, y.d, y.s, dS, s, 1, el(QKV, h, E), 3 * h, 0, EPI_STORE, dQKV, 3 * h);
+  batch_heads(g, y, y.a * ss, ss, s * 3 * h, d, s * 3 * h, d);
+  g.krange = y.causal ? KR_BELOW : KR_FULL;
+  HIPCHK(gemm(st, g));
+  // dK = dS^T Q
+  g = gp(y.s, y.d, y.s, dS, s, 0, QKV, 3 * h, 0, EPI_STORE, el(dQKV, h, E), 3 * h);
+  batch_heads(g, y, y.a * ss, ss, s * 3 * h, d, s * 3 * h, d);
+  g.krange = y.causal ? KR_ABOVE : KR_FULL;
+  HIPCHK(gemm(st, g));
+  // dV = P^T dO
+  g = gp(y.s, y.d, y.s, P, s, 0, dO, h, 0, EPI_STORE, el(dQKV, 2 * h, E), 3 * h);
+  batch_heads(g, y, y.a * ss, ss, s * h, d, s * 3 * h, d);
+  g.krange = y.causal ? KR_ABOVE : KR_FULL;
+  HIPCHK(gemm(st, g));
+  return RC_OK;
+}
+
+rc_status run_forward(rc_stage* st, int ws, int fs, const void* x, void* yout) {
+  const Layout& y = st->lay;
+  const int E = y.elt, L = y.L;
+  const long T = y.T, h = y.h, f = y.f;
+  hipStream_t s = st->stream;
+  HIPCHK(hipMemcpyAsync(wptr(st, ws, 0).X, x, T * h * E, hipMemcpyDeviceToDevice, s));
+  for (int l = 0; l < L; ++l) {
+    WPtr w = wptr(st, ws, l);
+    FPtr fl = fptr(st, fs, l);
+    HIPCHK(ln_forward(E, w.X, master(st, l, RC_P_LN1_G), master(st, l, RC_P_LN1_B), w.A, w.mu1,
+                      w.r1, T, y.h, y.eps, s));
+    GemmParams g = gp(T, 3 * h, h, w.A, h, 1, weight(st, l, RC_P_W_QKV), 3 * h, 0, EPI_BIAS, fl.QKV, 3 * h);
+    g.bias = master(st, l, RC_P_B_QKV);
+    HIPCHK(gemm(st, g));
+    rc_status r = attn_forward(st, fl.QKV, fl.P, w.O);
+    if (r != RC_OK) return r;
+    g = gp(T, h, h, w.O, h, 1, weight(st, l, RC_P_W_O), h, 0, EPI_BIAS_RESID, w.H, h);
+    g.bias = master(st, l, RC_P_B_O);
+    g.resid = w.X;
+    g.ld_resid = h;
+    HIPCHK(gemm(st, g));
+    HIPCHK(ln_forward(E, w.H, master(st, l, RC_P_LN2_G), master(st, l, RC_P_LN2_B), w.C, w.mu2,
+                      w.r2, T, y.h, y.eps, s));
+    g = gp(T, f, h, w.C, h, 1, weight(st, l, RC_P_W_1), f, 0, EPI_BIAS_GELU, fl.U, f);
+    g.bias = master(st, l, RC_P_B_1);
+    g.C2 = w.G;
+    g.ldc2 = f;
+    HIPCHK(gemm(st, g));
+    void* out = (l + 1 < L) ? (void*)wptr(st, ws, l + 1).X : yout;
+    g = gp(T, h, f, w.G, f, 1, weight(st, l, RC_P_W_2), h, 0, EPI_BIAS_RESID, out, h);
+    g.bias = master(st, l, RC_P_B_2);
+    g.resid = w.H;
+    g.ld_resid = h;
+    HIPCHK(gemm(st, g));
+  }
+  return RC_OK;
+}
+
+rc_status run_backward_input(rc_stage* st, int ws, int fs, const void* dy, void* dx) {
+  const Layout& y = st->lay;
+  const int E = y.elt, L = y.L;
+  const long T = y.T, h = y.h, f = y.f;
+  hipStream_t s = st->stream;
+  char* dO = st->work + y.off_dO;
+  HIPCHK(hipMemcpyAsync(wptr(st, ws, L - 1).dY, dy, T * h * E, hipMemcpyDeviceToDevice, s));
+  for (int l = L - 1; l >= 0; --l) {
+    WPtr w = wptr(st, ws, l);
+    FPtr fl = fptr(st, fs, l);
+    // dU = (dY W_2^T) * gelu'(U)
+    GemmParams g = gp(T, f, h, w.dY, h, 1, weight(st, l, RC_P_W_2), h, 1, EPI_GELU_BWD, w.dU, f);
+    g.aux = fl.U;
+    g.ld_aux = f;
+    HIPCHK(gemm(st, g));
+    // dC = dU W_1^T
+    g = gp(T, h, f, w.dU, f, 1, weight(st, l, RC_P_W_1), f, 1, EPI_STORE, w.dC, h);
+    HIPCHK(gemm(st, g));
+    // dH = dY + LN2^T(dC)
+    HIPCHK(ln_backward(E, w.dC, w.H, w.mu2, w.r2, master(st, l, RC_P_LN2_G), w.dY, w.dH, T, y.h, s));
+    // dO = dH W_o^T
+    g = gp(T, h, h, w.dH, h, 1, weight(st, l, RC_P_W_O), h, 1, EPI_STORE, dO, h);
+    HIPCHK(gemm(st, g));
+    rc_status r = attn_backward(st, fl.QKV, fl.P, dO, w.dQKV);
+    if (r != RC_OK) return r;
+    // dA = dQKV W_qkv^T
+    g = gp(T, h, 3 * h, w.dQKV, 3 * h, 1, weight(st, l, RC_P_W_QKV), 3 * h, 1, EPI_STORE, w.dA, h);
+    HIPCHK(gemm(st, g));
+    // dX = dH + LN1^T(dA)
+    void* out = l > 0 ? (void*)wptr(st, ws, l - 1).dY : dx;
+    HIPCHK(ln_backward(E, w.dA, w.X, w.mu1, w.r1, master(st, l, RC_P_LN1_G), w.dH, out, T, y.h, s));
+  }
+  return RC_OK;
+}
+
+rc_status run_backward_weight(rc_stage* st, int ws) {
+  const Layout& y = st->lay;
+  const int E = y.elt;
+  const long T = y.T, h = y.h, f = y.f;
+  const int acc = st->grads_fresh ? 0 : 1;
+  hipStream_t s = st->stream;
+  float* part = (float*)(st->work + y.off_part);
+  for (int l = 0; l < y.L; ++l) {
+    WPtr w = wptr(st, ws, l);
+    struct {
+      int pid;
+      long M, N;
+      char *X, *dY;
+    } lin[4] = {{RC_P_W_QKV, h, 3 * h, w.A, w.dQKV},
+                {RC_P_W_O, h, h, w.O, w.dH},
+                {RC_P_W_1, h, f, w.C, w.dU},
+                {RC_P_W_2, f, h, w.G, w.dY}};
+    for (auto& q : lin) {
+      // dW (+)= X^T dY : reduction over the T tokens
+      GemmParams g = gp(q.M, q.N, T, q.X, q.M, 0, q.dY, q.N, 0, EPI_F32_ACC, gradp(st, l, q.pid), q.N);
+      g.accumulate = acc;
+      HIPCHK(gemm(st, g));
+    }
+    HIPCHK(colsum_bias(E, w.dQKV, 3 * h, T, 3 * h, gradp(st, l, RC_P_B_QKV), acc, part, s));
+    HIPCHK(colsum_bias(E, w.dH, h, T, h, gradp(st, l, RC_P_B_O), acc, part, s));
+    HIPCHK(colsum_bias(E, w.dU, f, T, f, gradp(st, l, RC_P_B_1), acc, part, s));
+    HIPCHK(colsum_bias(E, w.dY, h, T, h, gradp(st, l, RC_P_B_2), acc, part, s));
+    HIPCHK(colsum_ln(E, w.dA, w.X, w.mu1, w.r1, T, h, gradp(st, l, RC_P_LN1_G),
+                     gradp(st, l, RC_P_LN1_B), acc, part, s));
+    HIPCHK(colsum_ln(E, w.dC, w.H, w.mu2, w.r2, T, h, gradp(st, l, RC_P_LN2_G),
+                     gradp(st, l, RC_P_LN2_B), acc, part, s));
+  }
+  return RC_OK;
+}
+
+rc_status run_optimizer(rc_stage* st, float grad_scale) {
+  const Layout& y = st->lay;
+  hipStream_t s = st->stream;
+  float* P = (float*)(st->state + y.off_master);
+  float* G = (float*)(st->state + y.off_grad);
+  float* M = (float*)(st->state + y.off_m);
+  float* V = (float*)(st->state + y.off_v);
+  if (st->grads_fresh) HIPCHK(fill_f32(G, y.n_total, 0.f, s));
+  const double t = (double)(st->t + 1);
+  const rc_adam_config& a = st->adam;
+  const double bc1 = 1.0 - std::pow((double)a.beta1, t);
+  const double bc2 = 1.0 - std::pow((double)a.beta2, t);
+  HIPCHK(adamw_step(P, G, M, V, y.bf ? (void*)(st->state + y.off_wb) : nullptr, y.n_total, y.n_mat,
+                    a.lr, a.beta1, a.beta2, a.eps, a.weight_decay, (float)(a.lr / bc1),
+                    (float)(1.0 / std::sqrt(bc2)), grad_scale, s));
+  return RC_OK;
+}
+
+void record(rc_stage* st, int op, int j, int k) {
+  rc_op_record r;
+  r.seq = (int64_t)st->log.size();
+  r.op = op;
+  r.j = j;
+  r.k = k;
+  r.k_s = st->pipeline_id;
+  r.stage = st->stage_index;
+  r.reserved = 0;
+  r.iter = st->iter;
+  st->log.push_back(r);
+}
+
+int take_min(std::vector<int>& v) {
+  auto it = std::min_element(v.begin(), v.end());
+  int x = *it;
+  v.erase(it);
+  return x;
+}
+
+rc_status check_param(rc_stage* st, int layer, int pid) {
+  if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
+  if (layer < 0 || layer >= st->lay.L) return fail(RC_ERR_INVALID_ARG, "layer out of range");
+  if (pid < 0 || pid >= RC_NUM_PARAMS) return fail(RC_ERR_INVALID_ARG, "param_id out of range");
+  if (st->dry) return fail(RC_ERR_INVALID_ARG, "dry-run handle has no device memory");
+  return RC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rc_status rc_stage_memory_requirements(const rc_stage_config* cfg, size_t* state_bytes,
+                                       size_t* stash_bytes, size_t* work_bytes) {
+  if (!state_bytes || !stash_bytes || !work_bytes) return fail(RC_ERR_INVALID_ARG, "null output pointer");
+  Layout y;
+  rc_status r = make_layout(cfg, y);
+  if (r != RC_OK) return r;
+  *state_bytes = y.state_bytes;
+  *stash_bytes = y.stash_bytes;
+  *work_bytes = y.work_bytes;
+  return RC_OK;
+}
+
+rc_status rc_stage_create(const rc_stage_config* cfg, const rc_adam_config* adam,
+                          int32_t stage_index, int32_t pipeline_id, void* state_arena,
+                          void* stash_arena, void* work_arena, void* hip_stream, rc_stage** out) {
+  if (!out || !adam) return fail(RC_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  Layout y;
+  rc_status r = make_layout(cfg, y);
+  if (r != RC_OK) return r;
+  const bool dry = !state_arena && !stash_arena && !work_arena;
+  if (!dry) {
+    if (!state_arena || !stash_arena || !work_arena)
+      return fail(RC_ERR_INVALID_ARG, "either all three arenas or none (dry run)");
+    if (((uintptr_t)state_arena | (uintptr_t)stash_arena | (uintptr_t)work_arena) % kAlign)
+      return fail(RC_ERR_INVALID_ARG, "arenas must be 256-byte aligned");
+  }
+  rc_stage* st = new rc_stage();
+  st->cfg = *cfg;
+  st->adam = *adam;
+  st->stage_index = stage_index;
+  st->pipeline_id = pipeline_id;
+  st->dry = dry;
+  st->stream = (hipStream_t)hip_stream;
+  st->state = (char*)state_arena;
+  st->stash = (char*)stash_arena;
+  st->work = (char*)work_arena;
+  st->lay = y;
+  for (int i = 0; i < y.wslots; ++i) st->free_w.push_back(i);
+  for (int i = 0; i < y.fslots; ++i) st->free_f.push_back(i);
+  if (!dry) {
+    hipError_t e = hipMemsetAsync(st->state, 0, y.state_bytes, st->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(st->stream);
+    if (e != hipSuccess) {
+      delete st;
+      return fail(RC_ERR_HIP, std::string("zeroing the state arena: ") + hipGetErrorString(e));
+    }
+  }
+  *out = st;
+  return RC_OK;
+}
+
+rc_status rc_stage_destroy(rc_stage* st) {
+  if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
+  hipError_t e = st->dry ? hipSuccess : hipStreamSynchronize(st->stream);
+  delete st;
+  if (e != hipSuccess) return fail(RC_ERR_HIP, std::string("destroy: ") + hipGetErrorString(e));
+  return RC_OK;
+}
+
+rc_status rc_stage_load_param(rc_stage* st, int32_t layer, int32_t param_id, const float* host_src) {
+  rc_status r = check_param(st, layer, param_id);
+  if (r != RC_OK) return r;
+  if (!host_src) return fail(RC_ERR_INVALID_ARG, "null host_src");
+  const PLoc& p = st->lay.p[layer][param_id];
+  float* dst = master(st, layer, param_id);
+  HIPCHK(hipMemcpyAsync(dst, host_src, 4 * p.count, hipMemcpyHostToDevice, st->stream));
+  const bool matrix = param_id == RC_P_W_QKV || param_id == RC_P_W_O || param_id == RC_P_W_1 ||
+                      param_id == RC_P_W_2;
+  if (st->lay.bf && matrix)
+    HIPCHK(cast_f32_to_bf16(dst, (char*)st->state + st->lay.off_wb + 2 * p.off, p.count, st->stream));
+  HIPCHK(hipStreamSynchronize(st->stream));
+  return RC_OK;
+}
+
+rc_status rc_stage_read(rc_stage* st, int32_t what, int32_t layer, int32_t param_id, float* host_dst) {
+  rc_status r = check_param(st, layer, param_id);
+  if (r != RC_OK) return r;
+  if (!host_dst) return fail(RC_ERR_INVALID_ARG, "null host_dst");
+  size_t base;
+  switch (what) {
+    case RC_READ_PARAM: base = st->lay.off_master; break;
+    case RC_READ_GRAD: base = st->lay.off_grad; break;
+    case RC_READ_ADAM_M: base = st->lay.off_m; break;
+    case RC_READ_ADAM_V: base = st->lay.off_v; break;
+    default: return fail(RC_ERR_INVALID_ARG, "unknown read target");
+  }
+  const PLoc& p = st->lay.p[layer][param_id];
+  HIPCHK(hipMemcpyAsync(host_dst, (float*)(st->state + base) + p.off, 4 * p.count,
+                        hipMemcpyDeviceToHost, st->stream));
+  HIPCHK(hipStreamSynchronize(st->stream));
+  return RC_OK;
+}
+
+rc_status rc_stage_forward(rc_stage* st, rc_mb mb, const void* x, void* y) {
+  if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
+  if (!st->dry && (!x || !y || x == y)) return fail(RC_ERR_INVALID_ARG, "x, y must be distinct device buffers");
+  auto key = std::make_pair(mb.j, mb.k);
+  if (st->mbs.count(key))
+    return fail(RC_ERR_BAD_STATE, "forward of micro-batch (" + std::to_string(mb.j) + "," +
+                                      std::to_string(mb.k) + ") already ran this iteration");
+  if (st->free_w.empty() || st->free_f.empty())
+    return fail(RC_ERR_OUT_OF_STASH, "no free stash slot for micro-batch (" + std::to_string(mb.j) +
+                                         "," + std::to_string(mb.k) + ")");
+  int ws = take_min(st->free_w), fs = take_min(st->free_f);
+  if (!st->dry) {
+    rc_status r = run_forward(st, ws, fs, x, y);
+    if (r != RC_OK) {
+      st->free_w.push_back(ws);
+      st->free_f.push_back(fs);
+      return r;
+    }
+  }
+  st->mbs[key] = {1, ws, fs};
+  record(st, RC_OP_F, mb.j, mb.k);
+  return RC_OK;
+}
+
+rc_status rc_stage_backward_input(rc_stage* st, rc_mb mb, const void* dy, void* dx) {
+  if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
+  if (!st->dry && (!dy || !dx || dy == dx)) return fail(RC_ERR_INVALID_ARG, "dy, dx must be distinct device buffers");
+  auto it = st->mbs.find(std::make_pair(mb.j, mb.k));
+  if (it == st->mbs.end() || it->second.state != 1)
+    return fail(RC_ERR_BAD_STATE, "backward_input of micro-batch (" + std::to_string(mb.j) + "," +
+                                      std::to_string(mb.k) + ") needs a completed forward and no prior B");
+  if (!st->dry) {
+    rc_status r = run_backward_input(st, it->second.ws, it->second.fs, dy, dx);
+    if (r != RC_OK) return r;
+  }
+  st->free_f.push_back(it->second.fs);
+  it->second.fs = -1;
+  it->second.state = 2;
+  record(st, RC_OP_B, mb.j, mb.k);
+  return RC_OK;
+}
+
+rc_status rc_stage_backward_weight(rc_stage* st, rc_mb mb) {
+  if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
+  auto it = st->mbs.find(std::make_pair(mb.j, mb.k));
+  if (it == st->mbs.end() || it->second.state != 2)
+    return fail(RC_ERR_BAD_STATE, "backward_weight of micro-batch (" + std::to_string(mb.j) + "," +
+                                      std::to_string(mb.k) + ") needs a completed B and no prior W");
+  if (!st->dry) {
+    rc_status r = run_backward_weight(st, it->second.ws);
+    if (r != RC_OK) return r;
+  }
+  st->free_w.push_back(it->second.ws);
+  it->second.ws = -1;
+  it->second.state = 3;
+  st->grads_fresh = false;
+  record(st, RC_OP_W, mb.j, mb.k);
+  return RC_OK;
+}
+
+rc_status rc_stage_optimizer_step(rc_stage* st, float grad_scale) {
+  if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
+  for (auto& kv : st->mbs)
+    if (kv.second.state != 3)
+      return fail(RC_ERR_BAD_STATE, "optimizer step while micro-batch (" +
+                                        std::to_string(kv.first.first) + "," +
+                                        std::to_string(kv.first.second) + ") has not run W");
+  if (!st->dry) {
+    rc_status r = run_optimizer(st, grad_scale);
+    if (r != RC_OK) return r;
+  }
+  st->t += 1;
+  record(st, RC_OP_STEP, -1, -1);
+  st->mbs.clear();
+  st->grads_fresh = true;
+  st->iter += 1;
+  return RC_OK;
+}
+
+rc_status rc_stage_op_log(rc_stage* st, rc_op_record* buf, int32_t cap, int32_t* n) {
+  if (!st || !n || (cap > 0 && !buf) || cap < 0) return fail(RC_ERR_INVALID_ARG, "bad op_log arguments");
+  *n = (int32_t)st->log.size();
+  const int32_t m = std::min<int32_t>(cap, *n);
+  if (m > 0) std::memcpy(buf, st->log.data(), sizeof(rc_op_record) * m);
+  return RC_OK;
+}
+
+rc_status rc_stage_stash_usage(rc_stage* st, int32_t* stashed, int32_t* inflight) {
+  if (!st || !stashed || !inflight) return fail(RC_ERR_INVALID_ARG, "null argument");
+  *stashed = st->lay.wslots - (int32_t)st->free_w.size();
+  *inflight = st->lay.fslots - (int32_t)st->free_f.size();
+  return RC_OK;
+}
+
+rc_status rc_stage_set_stream(rc_stage* st, void* hip_stream) {
+  if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
+  st->stream = (hipStream_t)hip_stream;
+  return RC_OK;
+}
+
+rc_status rc_stage_synchronize(rc_stage* st) {
+  if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
+  if (st->dry) return RC_OK;
+  HIPCHK(hipStreamSynchronize(st->stream));
+  HIPCHK(hipGetLastError());
+  return RC_OK;
+}
+
+const char* rc_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,161 @@
+"""CPU checks of the C-ABI library: it loads, exports every symbol the header
+declares, validates configurations, and its host bookkeeping (the
+micro-batch state machine, stash slots and op log of a dry-run handle)
+matches the oracle's on every workload's op list.  No compute call runs here.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from synth import CONFIGS, TEST_CONFIGS, MB, gen_params, get_config, op_list
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def lib_or_skip():
+    import paper_2405_14009_amd._lib as L
+    if not os.path.exists(L.LIB_PATH):
+        pytest.skip("library not built (run __graft_entry__.build())")
+    return L, L.load()
+
+
+def header_functions():
+    txt = open(os.path.join(ROOT, "include", "recycle_stage.h")).read()
+    return set(re.findall(r"^(?:rc_status|const char\*)\s+(rc_\w+)\s*\(", txt, re.M))
+
+
+def test_library_exports_every_declared_symbol():
+    L, lib = lib_or_skip()
+    declared = header_functions()
+    assert declared == set(L.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def _cfg(**kw):
+    import paper_2405_14009_amd._lib as L
+    base = dict(num_layers=1, hidden=256, heads=4, ffn=1024, seq_len=128, micro_batch=1, causal=1,
+                dtype=L.RC_FP32, ln_eps=1e-5, max_stashed_mb=4, max_inflight_mb=4)
+    base.update(kw)
+    return L.RcStageConfig(**base)
+
+
+def _req(cfg):
+    L, lib = lib_or_skip()
+    a, b, c = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+    st = lib.rc_stage_memory_requirements(ctypes.byref(cfg), ctypes.byref(a), ctypes.byref(b),
+                                          ctypes.byref(c))
+    return st, a.value, b.value, c.value
+
+
+def test_memory_requirements_and_validation():
+    L, lib = lib_or_skip()
+    st, state, stash, work = _req(_cfg())
+    assert st == 0 and state > 0 and stash > 0 and work > 0
+    # the stash is max_stashed weight-pass slots + max_inflight forward-only slots
+    _, _, stash2, _ = _req(_cfg(max_stashed_mb=8, max_inflight_mb=4))
+    _, _, stash3, _ = _req(_cfg(max_stashed_mb=8, max_inflight_mb=8))
+    wslot = (stash2 - stash) // 4
+    fslot = (stash3 - stash2) // 4
+    h, f, T, a, s = 256, 1024, 128, 4, 128
+    assert wslot >= 4 * (12 * T * h + 2 * T * f) and wslot < 4 * (12 * T * h + 2 * T * f) + 64 * 1024
+    assert fslot >= 4 * (3 * T * h + T * f + a * s * s)
+    assert _req(_cfg(hidden=250, heads=5))[0] == L.RC_ERR_UNSUPPORTED      # head_dim 50
+    assert _req(_cfg(hidden=256, heads=3))[0] == L.RC_ERR_UNSUPPORTED
+    assert _req(_cfg(seq_len=100))[0] == L.RC_ERR_UNSUPPORTED
+    assert _req(_cfg(dtype=7))[0] == L.RC_ERR_INVALID_ARG
+    assert _req(_cfg(max_inflight_mb=5))[0] == L.RC_ERR_INVALID_ARG
+    assert _req(_cfg(num_layers=0))[0] == L.RC_ERR_INVALID_ARG
+    assert lib.rc_stage_memory_requirements(None, None, None, None) == L.RC_ERR_INVALID_ARG
+    assert b"null" in lib.rc_last_error()
+
+
+def test_bf16_state_holds_weight_copies():
+    L, _ = lib_or_skip()
+    _, s32, _, _ = _req(_cfg(dtype=L.RC_FP32))
+    _, s16, _, _ = _req(_cfg(dtype=L.RC_BF16))
+    n_mat = 4 * 256 * 256 + 2 * 256 * 1024
+    assert s16 - s32 >= 2 * n_mat
+
+
+def _drive(stage, ops):
+    for op in ops:
+        if op.kind == "F":
+            stage.forward(op.mb)
+        elif op.kind == "B":
+            stage.backward_input(op.mb)
+        elif op.kind == "W":
+            stage.backward_weight(op.mb)
+        else:
+            stage.optimizer_step()
+
+
+@pytest.mark.parametrize("name", list(CONFIGS) + list(TEST_CONFIGS))
+def test_dry_run_op_log_matches_oracle(name):
+    lib_or_skip()
+    from paper_2405_14009_amd import Stage
+    cfg = get_config(name)
+    ops = op_list(cfg) * 2   # two iterations
+    st = Stage.from_config(cfg, dry_run=True, stage_index=3, pipeline_id=0)
+    _drive(st, ops)
+    ref = oracle_bookkeeping(cfg, ops)
+    assert st.op_log() == [(r[0], r[1], r[2], r[3], r[4], r[5]) for r in ref]
+
+
+def oracle_bookkeeping(cfg, ops):
+    """The oracle's state machine on the same op list, with the compute
+    replaced by no-ops (tiny placeholder tensors)."""
+    o = oracle.OracleStage(cfg.with_(layers=0), [], pipeline_id=0)
+    for op in ops:
+        if op.kind == "F":
+            o.forward(op.mb, np.zeros((1, 1, 1)))
+        elif op.kind == "B":
+            o.backward_input(op.mb, np.zeros((1, 1, 1)))
+        elif op.kind == "W":
+            o.backward_weight(op.mb)
+        else:
+            o.optimizer_step()
+    return [tuple(r) for r in o.log]
+
+
+def test_dry_run_error_table_matches_oracle():
+    lib_or_skip()
+    import paper_2405_14009_amd as P
+    cfg = get_config("tiny").with_(n_mb=3, max_stashed_mb=2, max_inflight_mb=1)
+    st = P.Stage.from_config(cfg, dry_run=True)
+    o = oracle.OracleStage(cfg.with_(layers=0), [])
+    z = np.zeros((1, 1, 1))
+    m0, m1, m2 = MB(0), MB(1), MB(2)
+    seq = [("B", m0), ("W", m0), ("F", m0), ("F", m0), ("W", m0), ("F", m1), ("B", m0),
+           ("B", m0), ("F", m1), ("F", m2), ("STEP", None), ("W", m0), ("W", m0), ("F", m0),
+           ("B", m1), ("W", m1), ("STEP", None), ("F", m0)]
+    codes = {P.BadStateError: "BAD_STATE", P.OutOfStashError: "OUT_OF_STASH"}
+    for kind, mb in seq:
+        got = want = "OK"
+        try:
+            {"F": lambda: st.forward(mb), "B": lambda: st.backward_input(mb),
+             "W": lambda: st.backward_weight(mb), "STEP": st.optimizer_step}[kind]()
+        except (P.BadStateError, P.OutOfStashError) as e:
+            got = codes[type(e)]
+        try:
+            {"F": lambda: o.forward(mb, z), "B": lambda: o.backward_input(mb, z),
+             "W": lambda: o.backward_weight(mb), "STEP": o.optimizer_step}[kind]()
+        except oracle.StageError as e:
+            want = e.code
+        assert got == want, (kind, mb)
+        assert st.stash_usage() == (o._n_stashed(), o._n_inflight())
+    assert st.op_log() == [tuple(r) for r in o.log]
+
+
+def test_product_fails_loudly_without_gpu():
+    lib_or_skip()
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    import paper_2405_14009_amd as P
+    with pytest.raises(RuntimeError, match="no HIP device"):
+        P.Stage.from_config(get_config("tiny"))
