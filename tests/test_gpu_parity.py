@@ -38,14 +38,29 @@ def _need_gpu():
 
 
 def compare_state(cfg, g, o, t, zero_init=()):
-    """grads after the last W, then params / m / v after the step."""
+    """grads after the last W, then params / m / v after the step.
+
+    The K block of the QKV bias has an exactly zero gradient (adding a
+    constant to every key of a query leaves its softmax unchanged), so both
+    sides hold rounding noise there and the first AdamW update is the sign of
+    that noise: its parameters are not compared; instead its gradient must be
+    negligible next to the V block's."""
     worst = {}
+    h = cfg.hidden
     for l in range(cfg.layers):
         for p in range(12):
             worst[("grad", l, p)] = rel_l2(g.grads[l][p], o.grads[l][p])
             worst[("m", l, p)] = rel_l2(g.m[l][p], o.stage.m[l][p])
             worst[("v", l, p)] = rel_l2(g.v[l][p], o.stage.v[l][p])
-            if (l, p) not in zero_init:
+            if (l, p) in zero_init:
+                continue
+            if p == 3:
+                keep = np.r_[0:h, 2 * h:3 * h]
+                worst[("param", l, p)] = rel_l2(g.params[l][p][keep], o.stage.params[l][p][keep])
+                ratio = np.linalg.norm(g.grads[l][p][h:2 * h]) / np.linalg.norm(g.grads[l][p][2 * h:])
+                log(f"  layer {l}: |grad b_k| / |grad b_v| = {ratio:.2e}")
+                assert ratio < (1e-4 if cfg.dtype == "f32" else 2e-2)
+            else:
                 worst[("param", l, p)] = rel_l2(g.params[l][p], o.stage.params[l][p])
     bad = {k: v for k, v in worst.items() if v > t}
     assert not bad, bad
@@ -154,10 +169,8 @@ def test_staggered_two_stages():
     r0 = run_gpu(cfg, [], stage=s0)
     o0 = oracle.run_oplist(cfg, params=p0)
     o1 = oracle.run_oplist(cfg, params=p1)
-    for st, r, o in ((0, r0, o0), (1, r1, o1)):
-        for l in range(cfg.layers):
-            for p in range(12):
-                assert rel_l2(r.params[l][p], o.stage.params[l][p]) < 1e-5, (st, l, p)
+    for r, o in ((r0, o0), (r1, o1)):
+        compare_state(cfg, r, o, 1e-5)
     s0.close()
     s1.close()
 
