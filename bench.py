@@ -1,0 +1,220 @@
+#!/usr/bin/env python3
+"""Benchmark one pipeline stage's decoupled-backprop training iteration on one MI355X.
+
+A step is one iteration of the stage's op list: every micro-batch's forward
+(F), input-gradient pass (B_input) and deferred weight-gradient pass
+(B_weight), then the stage's own AdamW step, on seeded synthetic inputs that
+are resident in HBM before the timed region.  The default workload is the
+GPT-6.7B-shaped stage (4 pre-LN layers, hidden 4096, 32 heads, FFN 16384,
+causal sequence 2048, micro-batch 1, 16 micro-batches with all weight passes
+deferred and issued in a shuffled order).
+
+Prints one JSON line: stage TFLOP/s (value), micro-batches/s, F/B/W TFLOP/s,
+GEMM-class TFLOP/s and their fraction of the bf16 MFMA peak, the roofline of
+the dominant kernel class, and the fp64 CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
+PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = "stage F/B/W TFLOP/s + % bf16 MFMA peak; micro-batches/sec per stage"
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def workload_name(cfg) -> str:
+    return (f"{cfg.name}-stage: {cfg.layers} pre-LN layers, hidden {cfg.hidden}, {cfg.heads} heads, "
+            f"ffn {cfg.ffn}, {'causal ' if cfg.causal else ''}seq {cfg.seq}, micro-batch "
+            f"{cfg.micro_batch}, {cfg.n_mb} micro-batches ({len(cfg.rerouted)} re-routed), "
+            f"schedule {cfg.schedule}, {cfg.dtype}")
+
+
+def cpu_baseline(cfg, params) -> dict:
+    """The fp64 oracle (as it stands) on a bounded sample of the workload:
+    F + B_input + B_weight of one layer for one micro-batch at full shape."""
+    import numpy as np
+    import oracle
+    from synth import gen_dy, gen_x
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    P = [p.astype(np.float64) for p in params[0]]
+    x = gen_x(cfg, 0).astype(np.float64)
+    dy = gen_dy(cfg, 0).astype(np.float64)
+    shp = oracle.LayerShape(cfg.heads, cfg.causal, cfg.ln_eps)
+    t0 = time.perf_counter()
+    y, cache = oracle.layer_forward(x, P, shp)
+    dx, ws = oracle.layer_backward_input(dy, cache, P)
+    oracle.layer_backward_weight(ws)
+    dt = time.perf_counter() - t0
+    flops = sum(cfg.flops_per_layer())
+    return {"value": round(flops / dt / 1e12, 4), "unit": "TFLOP/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": (f"fp64 numpy oracle: F + B_input + B_weight of 1 of {cfg.layers} layers for 1 of "
+                       f"{cfg.n_mb} micro-batches at full shape ({flops / 1e9:.0f} GFLOP algorithmic) "
+                       f"in {dt:.1f} s")}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="gpt6.7b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true",
+                    help="skip the per-kernel events (for external profilers)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one stage on one GPU; runs on more than one GPU are not part of "
+              "this build (use --gpus 1)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2405_14009_amd import Stage
+    from synth import get_config, gen_dy, gen_params, gen_x, op_list
+
+    def to_device(a, dtype):
+        t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to("cuda")
+        return t.to(torch.bfloat16) if dtype == "bf16" else t
+
+    if not torch.cuda.is_available():
+        print("no HIP device", file=sys.stderr)
+        return 1
+    cfg = get_config(args.config)
+    ops = op_list(cfg)
+    log(f"workload {workload_name(cfg)}")
+    t = time.perf_counter()
+    params = gen_params(cfg)
+    stage = Stage.from_config(cfg)
+    stage.load_params(params)
+    xs = {tuple(o.mb): to_device(gen_x(cfg, o.mb.j, o.mb.k), cfg.dtype) for o in ops if o.kind == "F"}
+    dys = {tuple(o.mb): to_device(gen_dy(cfg, o.mb.j, o.mb.k), cfg.dtype) for o in ops if o.kind == "F"}
+    ys = {k: torch.empty_like(v) for k, v in xs.items()}
+    dxs = {k: torch.empty_like(v) for k, v in xs.items()}
+    torch.cuda.synchronize()
+    log(f"setup {time.perf_counter() - t:.1f} s (stage arenas "
+        f"{(stage.state_bytes + stage.stash_bytes + stage.work_bytes) / 2**30:.1f} GiB)")
+
+    def run_step(events=None):
+        for op in ops:
+            if events is not None:
+                a = torch.cuda.Event(enable_timing=True)
+                a.record()
+            if op.kind == "F":
+                stage.forward(op.mb, xs[tuple(op.mb)], ys[tuple(op.mb)])
+            elif op.kind == "B":
+                stage.backward_input(op.mb, dys[tuple(op.mb)], dxs[tuple(op.mb)])
+            elif op.kind == "W":
+                stage.backward_weight(op.mb)
+            else:
+                stage.optimizer_step()
+            if events is not None:
+                b = torch.cuda.Event(enable_timing=True)
+                b.record()
+                events.append((op.kind, a, b))
+
+    for i in range(args.warmup):
+        run_step()
+        torch.cuda.synchronize()
+        log(f"warmup step {i + 1}/{args.warmup} done")
+
+    profile = not args.no_profile
+    events = [] if profile else None
+    if profile:
+        stage.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        run_step(events)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    log(f"timed {args.steps} steps in {wall:.3f} s")
+    stage.synchronize()
+
+    F, B, W = cfg.flops_per_layer()
+    it_flops = cfg.layers * cfg.n_mb * (F + B + W)
+    ms_per_step = 1e3 * wall / args.steps
+    out = {
+        "metric": METRIC,
+        "value": round(it_flops * args.steps / wall / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) activations, N(0,1e-2) upstream gradients)",
+        "config": {"workload": workload_name(cfg), "layers": cfg.layers, "hidden": cfg.hidden,
+                   "heads": cfg.heads, "ffn": cfg.ffn, "seq_len": cfg.seq,
+                   "micro_batch": cfg.micro_batch, "micro_batches": cfg.n_mb,
+                   "tokens_per_micro_batch": cfg.tokens, "parallelism": "one stage, one GPU"},
+        "mb_per_s": round(cfg.n_mb * args.steps / wall, 2),
+        "pct_bf16_peak": round(100 * it_flops * args.steps / wall / 1e12 / PEAK_BF16_TFLOPS, 2),
+    }
+    if profile:
+        per = {"F": 0.0, "B": 0.0, "W": 0.0, "STEP": 0.0}
+        for kind, a, b in events:
+            per[kind] += a.elapsed_time(b)
+        nl = cfg.layers * cfg.n_mb * args.steps
+        out["pass_tflops"] = {k: round(nl * fl / (per[k] / 1e3) / 1e12, 2)
+                              for k, fl in (("F", F), ("B", B), ("W", W))}
+        out["pass_ms_per_mb"] = {k: round(per[k] / (cfg.n_mb * args.steps), 3) for k in ("F", "B", "W")}
+        out["optimizer_ms"] = round(per["STEP"] / args.steps, 3)
+        prof = stage.profile_read()
+        stage.profile_enable(False)
+        kern = {}
+        for name, r in prof.items():
+            if r["launches"] == 0 or r["ms"] <= 0:
+                continue
+            e = {"launches": r["launches"], "avg_us": round(1e3 * r["ms"] / r["launches"], 2),
+                 "share_pct": 0.0}
+            if r["flops"] > 0:
+                e["tflops"] = round(r["flops"] / (r["ms"] / 1e3) / 1e12, 2)
+                e["pct_bf16_peak"] = round(100 * e["tflops"] / PEAK_BF16_TFLOPS, 2)
+            if r["bytes"] > 0:
+                e["gbs"] = round(r["bytes"] / (r["ms"] / 1e3) / 1e9, 1)
+            kern[name] = e
+        tot = sum(r["ms"] for r in prof.values())
+        for name in kern:
+            kern[name]["share_pct"] = round(100 * prof[name]["ms"] / tot, 1)
+        out["kernels"] = kern
+        dom = max(("gemm_fwd", "gemm_dgrad", "gemm_wgrad"), key=lambda n: prof[n]["ms"])
+        r = prof[dom]
+        achieved = r["flops"] / (r["ms"] / 1e3) / 1e12
+        out["roofline"] = {"kernel": f"{dom} (bf16 MFMA GEMM)", "bound": "mfma",
+                           "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                           "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                           "traffic": None,
+                           "avg_launch_us": round(1e3 * r["ms"] / r["launches"], 2),
+                           "flops_per_launch": r["flops"] / r["launches"]}
+    if not args.no_cpu_baseline:
+        log("timing the fp64 CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(cfg, params)
+    stage.close()
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -200,6 +200,43 @@ rc_status rc_stage_stash_usage(rc_stage* st, int32_t* stashed, int32_t* inflight
 /* Replace the handle's stream (subsequent calls enqueue on it). */
 rc_status rc_stage_set_stream(rc_stage* st, void* hip_stream);
 
+/* Kernel classes of the per-kernel profile (the per-op latencies the paper's
+ * Profiler collects for its Planner, section 4.1: T_F, T_B_input, T_B_weight,
+ * here broken down by kernel). */
+enum {
+  RC_K_GEMM_FWD = 0,    /* forward linear GEMMs: QKV, out-proj, FC1, FC2 */
+  RC_K_GEMM_DGRAD = 1,  /* input-gradient linear GEMMs (B_input) */
+  RC_K_GEMM_WGRAD = 2,  /* weight-gradient linear GEMMs (B_weight) */
+  RC_K_ATTN_FWD = 3,    /* attention core forward (one region per layer) */
+  RC_K_ATTN_BWD = 4,    /* attention core backward (one region per layer) */
+  RC_K_LN = 5,          /* LayerNorm forward / input-gradient kernels */
+  RC_K_REDUCE = 6,      /* bias and LayerNorm-affine gradient reductions */
+  RC_K_ADAM = 7,        /* fused AdamW */
+  RC_K_COPY = 8,        /* stage input / upstream gradient copied into the stash */
+  RC_K_COUNT = 9
+};
+
+/* Accumulated profile of one kernel class: number of timed regions, their
+ * total device time (HIP events on the handle's stream around each launch or
+ * region), and the algorithmic flops and HBM bytes of those regions
+ * (operands read + results written once, independent of the kernel design). */
+typedef struct rc_kernel_stat {
+  int32_t kind;
+  int32_t launches;
+  double ms;
+  double flops;
+  double bytes;
+} rc_kernel_stat;
+
+/* enable = 1: reset the profile and start recording events around every
+ * launch of subsequent calls; enable = 0: stop.  Host-side events only; no
+ * device memory.  Errors: RC_ERR_INVALID_ARG (null / dry-run handle), RC_ERR_HIP. */
+rc_status rc_stage_profile_enable(rc_stage* st, int32_t enable);
+
+/* Wait for the stream and copy the RC_K_COUNT class profiles into out
+ * (out[i].kind == i).  Errors: RC_ERR_INVALID_ARG, RC_ERR_HIP. */
+rc_status rc_stage_profile_read(rc_stage* st, rc_kernel_stat* out);
+
 /* Wait for the handle's stream; reports any deferred device error as RC_ERR_HIP. */
 rc_status rc_stage_synchronize(rc_stage* st);
 

@@ -22,8 +22,11 @@ EXPORTED = (
     "rc_stage_memory_requirements", "rc_stage_create", "rc_stage_destroy", "rc_stage_load_param",
     "rc_stage_read", "rc_stage_forward", "rc_stage_backward_input", "rc_stage_backward_weight",
     "rc_stage_optimizer_step", "rc_stage_op_log", "rc_stage_stash_usage", "rc_stage_set_stream",
-    "rc_stage_synchronize", "rc_last_error",
+    "rc_stage_synchronize", "rc_stage_profile_enable", "rc_stage_profile_read", "rc_last_error",
 )
+
+KERNEL_CLASSES = ("gemm_fwd", "gemm_dgrad", "gemm_wgrad", "attn_fwd", "attn_bwd", "layernorm",
+                  "reduce", "adamw", "copy")
 
 
 class RcStageConfig(ctypes.Structure):
@@ -47,6 +50,11 @@ class RcOpRecord(ctypes.Structure):
     _fields_ = [("seq", ctypes.c_int64), ("op", ctypes.c_int32), ("j", ctypes.c_int32),
                 ("k", ctypes.c_int32), ("k_s", ctypes.c_int32), ("stage", ctypes.c_int32),
                 ("reserved", ctypes.c_int32), ("iter", ctypes.c_int64)]
+
+
+class RcKernelStat(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("launches", ctypes.c_int32), ("ms", ctypes.c_double),
+                ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
 
 
 class RcError(RuntimeError):
@@ -98,6 +106,8 @@ def load() -> ctypes.CDLL:
         "rc_stage_stash_usage": [P, ctypes.POINTER(I32), ctypes.POINTER(I32)],
         "rc_stage_set_stream": [P, P],
         "rc_stage_synchronize": [P],
+        "rc_stage_profile_enable": [P, I32],
+        "rc_stage_profile_read": [P, ctypes.POINTER(RcKernelStat)],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)

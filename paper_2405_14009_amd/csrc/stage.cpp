@@ -194,6 +194,16 @@ struct rc_stage {
   std::vector<rc_op_record> log;
   int64_t iter = 0, t = 0;
   bool grads_fresh = true;
+  // per-kernel profile
+  struct Rec {
+    int kind;
+    hipEvent_t a, b;
+    double flops, bytes;
+  };
+  bool prof = false;
+  std::vector<Rec> pending;
+  std::vector<hipEvent_t> pool;
+  rc_kernel_stat stats[RC_K_COUNT];
 };
 
 namespace {
@@ -236,6 +246,37 @@ const void* weight(rc_stage* st, int l, int pid) {
 // Element offset into an activation buffer.
 inline char* el(void* p, long n, int elt) { return (char*)p + n * elt; }
 
+// Records a HIP event pair around the enclosed launches when profiling.
+struct Prof {
+  rc_stage* st;
+  int kind;
+  double flops, bytes;
+  hipEvent_t a = nullptr;
+  Prof(rc_stage* s, int k, double fl, double by) : st(s), kind(k), flops(fl), bytes(by) {
+    if (st->prof) a = next_event(st);
+  }
+  ~Prof() {
+    if (!st->prof || !a) return;
+    hipEvent_t b = next_event(st);
+    if (b) st->pending.push_back({kind, a, b, flops, bytes});
+  }
+  static hipEvent_t next_event(rc_stage* st) {
+    hipEvent_t e = nullptr;
+    if (!st->pool.empty()) {
+      e = st->pool.back();
+      st->pool.pop_back();
+    } else if (hipEventCreate(&e) != hipSuccess) {
+      return nullptr;
+    }
+    hipEventRecord(e, st->stream);
+    return e;
+  }
+};
+
+double gemm_bytes(long M, long N, long K, int in_elt, int out_bytes) {
+  return (double)in_elt * ((double)M * K + (double)K * N) + (double)out_bytes * M * N;
+}
+
 GemmParams gp(int M, int N, int K, const void* A, long lda, int ak, const void* B, long ldb, int bk,
               int epi, void* C, long ldc) {
   GemmParams g;
@@ -259,6 +300,17 @@ GemmParams gp(int M, int N, int K, const void* A, long lda, int ak, const void* 
 
 hipError_t gemm(rc_stage* st, const GemmParams& g) {
   return st->lay.bf ? gemm_bf16(g, st->stream) : gemm_f32(g, st->stream);
+}
+
+// A linear-layer GEMM, profiled as one launch of class `kind`.
+hipError_t gemm_lin(rc_stage* st, const GemmParams& g, int kind) {
+  const int E = st->lay.elt;
+  int ob = E;
+  if (g.epi == EPI_F32_ACC) ob = g.accumulate ? 8 : 4;
+  if (g.epi == EPI_BIAS_GELU) ob = 2 * E;
+  if (g.epi == EPI_BIAS_RESID || g.epi == EPI_GELU_BWD) ob = 2 * E;
+  Prof pr(st, kind, 2.0 * g.M * (double)g.N * g.K, gemm_bytes(g.M, g.N, g.K, E, ob));
+  return gemm(st, g);
 }
 
 // Per (sequence, head) batching of the attention products; Q, K, V and dQ,
@@ -329,35 +381,49 @@ rc_status run_forward(rc_stage* st, int ws, int fs, const void* x, void* yout) {
   const int E = y.elt, L = y.L;
   const long T = y.T, h = y.h, f = y.f;
   hipStream_t s = st->stream;
-  HIPCHK(hipMemcpyAsync(wptr(st, ws, 0).X, x, T * h * E, hipMemcpyDeviceToDevice, s));
+  {
+    Prof pr(st, RC_K_COPY, 0, 2.0 * T * h * E);
+    HIPCHK(hipMemcpyAsync(wptr(st, ws, 0).X, x, T * h * E, hipMemcpyDeviceToDevice, s));
+  }
+  const double ln_f_bytes = 2.0 * T * h * E + 8.0 * T + 8.0 * h;
+  const double att = (y.causal ? 1.0 : 2.0) * y.b * (double)y.s * y.s * h;
   for (int l = 0; l < L; ++l) {
     WPtr w = wptr(st, ws, l);
     FPtr fl = fptr(st, fs, l);
-    HIPCHK(ln_forward(E, w.X, master(st, l, RC_P_LN1_G), master(st, l, RC_P_LN1_B), w.A, w.mu1,
-                      w.r1, T, y.h, y.eps, s));
+    {
+      Prof pr1(st, RC_K_LN, 0, ln_f_bytes);
+      HIPCHK(ln_forward(E, w.X, master(st, l, RC_P_LN1_G), master(st, l, RC_P_LN1_B), w.A, w.mu1,
+                        w.r1, T, y.h, y.eps, s));
+    }
     GemmParams g = gp(T, 3 * h, h, w.A, h, 1, weight(st, l, RC_P_W_QKV), 3 * h, 0, EPI_BIAS, fl.QKV, 3 * h);
     g.bias = master(st, l, RC_P_B_QKV);
-    HIPCHK(gemm(st, g));
-    rc_status r = attn_forward(st, fl.QKV, fl.P, w.O);
-    if (r != RC_OK) return r;
+    HIPCHK(gemm_lin(st, g, RC_K_GEMM_FWD));
+    {
+      Prof pa(st, RC_K_ATTN_FWD, 2.0 * att, 4.0 * T * h * E);
+      rc_status r = attn_forward(st, fl.QKV, fl.P, w.O);
+      if (r != RC_OK) return r;
+    }
     g = gp(T, h, h, w.O, h, 1, weight(st, l, RC_P_W_O), h, 0, EPI_BIAS_RESID, w.H, h);
     g.bias = master(st, l, RC_P_B_O);
     g.resid = w.X;
     g.ld_resid = h;
-    HIPCHK(gemm(st, g));
-    HIPCHK(ln_forward(E, w.H, master(st, l, RC_P_LN2_G), master(st, l, RC_P_LN2_B), w.C, w.mu2,
-                      w.r2, T, y.h, y.eps, s));
+    HIPCHK(gemm_lin(st, g, RC_K_GEMM_FWD));
+    {
+      Prof pr2(st, RC_K_LN, 0, ln_f_bytes);
+      HIPCHK(ln_forward(E, w.H, master(st, l, RC_P_LN2_G), master(st, l, RC_P_LN2_B), w.C, w.mu2,
+                        w.r2, T, y.h, y.eps, s));
+    }
     g = gp(T, f, h, w.C, h, 1, weight(st, l, RC_P_W_1), f, 0, EPI_BIAS_GELU, fl.U, f);
     g.bias = master(st, l, RC_P_B_1);
     g.C2 = w.G;
     g.ldc2 = f;
-    HIPCHK(gemm(st, g));
+    HIPCHK(gemm_lin(st, g, RC_K_GEMM_FWD));
     void* out = (l + 1 < L) ? (void*)wptr(st, ws, l + 1).X : yout;
     g = gp(T, h, f, w.G, f, 1, weight(st, l, RC_P_W_2), h, 0, EPI_BIAS_RESID, out, h);
     g.bias = master(st, l, RC_P_B_2);
     g.resid = w.H;
     g.ld_resid = h;
-    HIPCHK(gemm(st, g));
+    HIPCHK(gemm_lin(st, g, RC_K_GEMM_FWD));
   }
   return RC_OK;
 }
@@ -368,7 +434,12 @@ rc_status run_backward_input(rc_stage* st, int ws, int fs, const void* dy, void*
   const long T = y.T, h = y.h, f = y.f;
   hipStream_t s = st->stream;
   char* dO = st->work + y.off_dO;
-  HIPCHK(hipMemcpyAsync(wptr(st, ws, L - 1).dY, dy, T * h * E, hipMemcpyDeviceToDevice, s));
+  {
+    Prof pr(st, RC_K_COPY, 0, 2.0 * T * h * E);
+    HIPCHK(hipMemcpyAsync(wptr(st, ws, L - 1).dY, dy, T * h * E, hipMemcpyDeviceToDevice, s));
+  }
+  const double ln_b_bytes = 4.0 * T * h * E + 8.0 * T + 4.0 * h;
+  const double att = (y.causal ? 1.0 : 2.0) * y.b * (double)y.s * y.s * h;
   for (int l = L - 1; l >= 0; --l) {
     WPtr w = wptr(st, ws, l);
     FPtr fl = fptr(st, fs, l);
@@ -376,22 +447,29 @@ rc_status run_backward_input(rc_stage* st, int ws, int fs, const void* dy, void*
     GemmParams g = gp(T, f, h, w.dY, h, 1, weight(st, l, RC_P_W_2), h, 1, EPI_GELU_BWD, w.dU, f);
     g.aux = fl.U;
     g.ld_aux = f;
-    HIPCHK(gemm(st, g));
+    HIPCHK(gemm_lin(st, g, RC_K_GEMM_DGRAD));
     // dC = dU W_1^T
     g = gp(T, h, f, w.dU, f, 1, weight(st, l, RC_P_W_1), f, 1, EPI_STORE, w.dC, h);
-    HIPCHK(gemm(st, g));
+    HIPCHK(gemm_lin(st, g, RC_K_GEMM_DGRAD));
     // dH = dY + LN2^T(dC)
-    HIPCHK(ln_backward(E, w.dC, w.H, w.mu2, w.r2, master(st, l, RC_P_LN2_G), w.dY, w.dH, T, y.h, s));
+    {
+      Prof pr(st, RC_K_LN, 0, ln_b_bytes);
+      HIPCHK(ln_backward(E, w.dC, w.H, w.mu2, w.r2, master(st, l, RC_P_LN2_G), w.dY, w.dH, T, y.h, s));
+    }
     // dO = dH W_o^T
     g = gp(T, h, h, w.dH, h, 1, weight(st, l, RC_P_W_O), h, 1, EPI_STORE, dO, h);
-    HIPCHK(gemm(st, g));
-    rc_status r = attn_backward(st, fl.QKV, fl.P, dO, w.dQKV);
-    if (r != RC_OK) return r;
+    HIPCHK(gemm_lin(st, g, RC_K_GEMM_DGRAD));
+    {
+      Prof pa(st, RC_K_ATTN_BWD, 4.0 * att, 8.0 * T * h * E);
+      rc_status r = attn_backward(st, fl.QKV, fl.P, dO, w.dQKV);
+      if (r != RC_OK) return r;
+    }
     // dA = dQKV W_qkv^T
     g = gp(T, h, 3 * h, w.dQKV, 3 * h, 1, weight(st, l, RC_P_W_QKV), 3 * h, 1, EPI_STORE, w.dA, h);
-    HIPCHK(gemm(st, g));
+    HIPCHK(gemm_lin(st, g, RC_K_GEMM_DGRAD));
     // dX = dH + LN1^T(dA)
     void* out = l > 0 ? (void*)wptr(st, ws, l - 1).dY : dx;
+    Prof pr(st, RC_K_LN, 0, ln_b_bytes);
     HIPCHK(ln_backward(E, w.dA, w.X, w.mu1, w.r1, master(st, l, RC_P_LN1_G), w.dH, out, T, y.h, s));
   }
   return RC_OK;
@@ -418,8 +496,10 @@ rc_status run_backward_weight(rc_stage* st, int ws) {
       // dW (+)= X^T dY : reduction over the T tokens
       GemmParams g = gp(q.M, q.N, T, q.X, q.M, 0, q.dY, q.N, 0, EPI_F32_ACC, gradp(st, l, q.pid), q.N);
       g.accumulate = acc;
-      HIPCHK(gemm(st, g));
+      HIPCHK(gemm_lin(st, g, RC_K_GEMM_WGRAD));
     }
+    const double rb = acc ? 8.0 : 4.0;
+    Prof pr(st, RC_K_REDUCE, 0, (double)T * (6 * h + f) * E + rb * (6 * h + f) + 2.0 * T * h * E + 16.0 * T + 4 * rb * h);
     HIPCHK(colsum_bias(E, w.dQKV, 3 * h, T, 3 * h, gradp(st, l, RC_P_B_QKV), acc, part, s));
     HIPCHK(colsum_bias(E, w.dH, h, T, h, gradp(st, l, RC_P_B_O), acc, part, s));
     HIPCHK(colsum_bias(E, w.dU, f, T, f, gradp(st, l, RC_P_B_1), acc, part, s));
@@ -444,6 +524,7 @@ rc_status run_optimizer(rc_stage* st, float grad_scale) {
   const rc_adam_config& a = st->adam;
   const double bc1 = 1.0 - std::pow((double)a.beta1, t);
   const double bc2 = 1.0 - std::pow((double)a.beta2, t);
+  Prof pr(st, RC_K_ADAM, 0, 28.0 * y.n_total + (y.bf ? 2.0 * y.n_mat : 0.0));
   HIPCHK(adamw_step(P, G, M, V, y.bf ? (void*)(st->state + y.off_wb) : nullptr, y.n_total, y.n_mat,
                     a.lr, a.beta1, a.beta2, a.eps, a.weight_decay, (float)(a.lr / bc1),
                     (float)(1.0 / std::sqrt(bc2)), grad_scale, s));
@@ -520,6 +601,7 @@ rc_status rc_stage_create(const rc_stage_config* cfg, const rc_adam_config* adam
   st->stash = (char*)stash_arena;
   st->work = (char*)work_arena;
   st->lay = y;
+  for (int i = 0; i < RC_K_COUNT; ++i) st->stats[i] = {i, 0, 0.0, 0.0, 0.0};
   for (int i = 0; i < y.wslots; ++i) st->free_w.push_back(i);
   for (int i = 0; i < y.fslots; ++i) st->free_f.push_back(i);
   if (!dry) {
@@ -537,6 +619,11 @@ rc_status rc_stage_create(const rc_stage_config* cfg, const rc_adam_config* adam
 rc_status rc_stage_destroy(rc_stage* st) {
   if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
   hipError_t e = st->dry ? hipSuccess : hipStreamSynchronize(st->stream);
+  for (auto& r : st->pending) {
+    st->pool.push_back(r.a);
+    st->pool.push_back(r.b);
+  }
+  for (hipEvent_t ev : st->pool) hipEventDestroy(ev);
   delete st;
   if (e != hipSuccess) return fail(RC_ERR_HIP, std::string("destroy: ") + hipGetErrorString(e));
   return RC_OK;
@@ -681,6 +768,40 @@ rc_status rc_stage_synchronize(rc_stage* st) {
   if (st->dry) return RC_OK;
   HIPCHK(hipStreamSynchronize(st->stream));
   HIPCHK(hipGetLastError());
+  return RC_OK;
+}
+
+rc_status rc_stage_profile_enable(rc_stage* st, int32_t enable) {
+  if (!st || st->dry) return fail(RC_ERR_INVALID_ARG, "profiling needs a device handle");
+  if (enable) {
+    HIPCHK(hipStreamSynchronize(st->stream));
+    for (auto& r : st->pending) {
+      st->pool.push_back(r.a);
+      st->pool.push_back(r.b);
+    }
+    st->pending.clear();
+    for (int i = 0; i < RC_K_COUNT; ++i) st->stats[i] = {i, 0, 0.0, 0.0, 0.0};
+  }
+  st->prof = enable != 0;
+  return RC_OK;
+}
+
+rc_status rc_stage_profile_read(rc_stage* st, rc_kernel_stat* out) {
+  if (!st || st->dry || !out) return fail(RC_ERR_INVALID_ARG, "profiling needs a device handle");
+  HIPCHK(hipStreamSynchronize(st->stream));
+  for (auto& r : st->pending) {
+    float ms = 0.f;
+    HIPCHK(hipEventElapsedTime(&ms, r.a, r.b));
+    rc_kernel_stat& k = st->stats[r.kind];
+    k.launches += 1;
+    k.ms += ms;
+    k.flops += r.flops;
+    k.bytes += r.bytes;
+    st->pool.push_back(r.a);
+    st->pool.push_back(r.b);
+  }
+  st->pending.clear();
+  for (int i = 0; i < RC_K_COUNT; ++i) out[i] = st->stats[i];
   return RC_OK;
 }
 

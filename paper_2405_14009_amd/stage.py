@@ -188,5 +188,16 @@ class Stage:
         self.stream = stream
         L.check(self._lib.rc_stage_set_stream(self._h, ctypes.c_void_p(stream.cuda_stream)))
 
+    def profile_enable(self, enable: bool = True) -> None:
+        """Start (resetting the counters) or stop the per-kernel-class profile."""
+        L.check(self._lib.rc_stage_profile_enable(self._h, 1 if enable else 0))
+
+    def profile_read(self) -> dict:
+        """{class: {launches, ms, flops, bytes}} accumulated since profile_enable()."""
+        buf = (L.RcKernelStat * len(L.KERNEL_CLASSES))()
+        L.check(self._lib.rc_stage_profile_read(self._h, buf))
+        return {L.KERNEL_CLASSES[r.kind]: dict(launches=r.launches, ms=r.ms, flops=r.flops,
+                                               bytes=r.bytes) for r in buf}
+
     def synchronize(self) -> None:
         L.check(self._lib.rc_stage_synchronize(self._h))
