@@ -1,245 +1,201 @@
 // bf16 GEMM kernel template on CDNA4 matrix cores: v_mfma_f32_32x32x16_bf16,
 // fp32 accumulate.
 //
-// Each wave owns a 128 x 64 output tile (4 x 2 MFMA blocks of 32x32, 128
-// accumulators); a workgroup tile of BM x BN uses (BM/128) x (BN/64) waves,
-// so a 256x256 tile runs 8 waves (two per SIMD, which hide each other's LDS
-// and memory latency) and a 256x128 tile 4 waves.
-// Operands are staged in LDS as [rows][64] k-contiguous tiles whose 16-byte
-// chunks are XOR-swizzled so fragment reads and tile writes spread over the
-// banks, double buffered along k with one barrier per 64-wide k-tile:
-// global loads of tile t+1 are in flight while the MFMAs of tile t run, and
-// within a tile the fragments of the next 16-wide k-step are read from LDS
-// while the current step's MFMAs issue.
-// Global loads are buffer loads whose out-of-range offsets return zero, so
-// ragged edges need no branches.  An operand that is contiguous along M/N in
-// memory (the token reduction of the weight-gradient GEMMs, the [in, out]
-// weights of the forward) is read in 16-byte vectors along M/N and
-// transposed 8x8 in registers before the LDS write, so MFMA fragments are
-// always k-contiguous.
+// Tiles.  Each wave owns a 128 x 64 output tile (4 x 2 MFMA blocks of 32x32,
+// 128 accumulators); a BM x BN workgroup tile uses (BM/128) x (BN/64) waves:
+// 256x256 runs 8 waves (two per SIMD, hiding each other's latencies),
+// 256x128 runs 4.
+//
+// Staging.  k-tiles of 64 are copied from memory straight into LDS by
+// buffer-load-to-LDS instructions (each wave instruction deposits 64 lanes x
+// 16 bytes contiguously; out-of-range offsets deposit zeros, so ragged edges
+// need no branches and no registers hold tile data).  Two LDS stages: the
+// copy of tile t+1 is in flight while tile t is multiplied, one barrier per
+// k-tile.
+//   * k-contiguous operand: LDS tile [rows][64], 16-byte chunks XOR-swizzled
+//     by row; fragments are one ds_read_b128 per lane.
+//   * m/n-contiguous operand (the token reduction of the weight-gradient
+//     GEMMs, the [in, out] weights in the forward): LDS tile [64][rows] in
+//     memory order, chunks XOR-swizzled by k-row; fragments are two
+//     ds_read_b64_tr_b16 per lane, which transpose 4x16 blocks across each
+//     16-lane group so every lane receives 8 k-consecutive values of its
+//     row/column, the same operand layout as the k-contiguous case.
+// Within a k-tile the fragments of the next 16-wide k-step are read while the
+// current step's MFMAs issue.
 #pragma once
-
-#include <type_traits>
 
 #include "gemm.h"
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
 
 namespace {
 
 constexpr int BK = 64;
-constexpr uint32_t kOOB = 0x80000000u;  // buffer offset that is always out of range -> loads 0
+constexpr uint32_t kOOB = 0x80000000u;  // buffer offset that is always out of range -> zeros
 
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 7; }
+// k-contiguous tiles: chunk c (8 elements) of row r lives at chunk c ^ swz_k(r).
+__device__ __forceinline__ int swz_k(int r) { return ((r >> 1) ^ (r >> 3)) & 7; }
+// m/n-contiguous tiles: chunk c of k-row r lives at chunk c ^ swz_mn(r).
+__device__ __forceinline__ int swz_mn(int r) { return (r & 3) << 2; }
 
-// Element offset of the 8-element chunk c of row r in a [rows][64] tile.
-__device__ __forceinline__ int lds_off(int r, int c) { return r * BK + ((c ^ swz(r)) << 3); }
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
-// Buffer descriptor over [base, base + bytes); base and size are workgroup
-// uniform, and are made provably so (readfirstlane) so that the descriptor
-// lives in scalar registers.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, long bytes) {
+// Buffer descriptor (4 dwords: base, stride 0, size in bytes, format) over
+// [base, base + bytes).  Base and size are workgroup uniform and made provably
+// so (readfirstlane), so the descriptor lives in scalar registers.
+__device__ __forceinline__ i32x4 make_rsrc(const void* base, long bytes) {
   const long cap = 0x7fffffffL;
   const uint64_t a = (uint64_t)base;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
-  const int n = __builtin_amdgcn_readfirstlane((int)(bytes < cap ? bytes : cap));
-  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), (short)0, n, 0x00020000);
+  i32x4 r;
+  r.x = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  r.y = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)) & 0xffff;
+  r.z = __builtin_amdgcn_readfirstlane((int)(bytes < cap ? bytes : cap));
+  r.w = 0x00020000;
+  return r;
 }
 
-__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+// 16 bytes per lane from buffer offset `off` into LDS at lds_base + 16 * lane
+// (zeros when off is out of range).  Issued as inline assembly so that the
+// compiler does not order later LDS reads of the other stage behind it; the
+// kernel waits for it explicitly (vmcnt) before the barrier that publishes
+// the stage.  M0 carries the LDS base and is not otherwise used by these
+// kernels.
+__device__ __forceinline__ void dma16(const i32x4& r, uint32_t lds_base, uint32_t off) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds_base), "v"(off), "s"(r)
+               : "memory", "m0");
 }
 
-__device__ __forceinline__ uint32_t comp(const uint4& u, int i) {
-  return i == 0 ? u.x : (i == 1 ? u.y : (i == 2 ? u.z : u.w));
+__device__ __forceinline__ uint32_t lds_addr(const char* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
 }
 
-// Tile of ROWS rows (m or n) x 64 k from a k-contiguous matrix: element
-// (r, k) at base[r * ld + k].  Thread t loads 16-byte chunks t, t+NT, ...
-template <int ROWS, int NT>
-struct LoadK {
-  static constexpr int NV = ROWS * 8 / NT;
-  static_assert(NV >= 1, "tile too small for the workgroup");
-  uint4 v[NV];
-  uint32_t row_off[NV];  // byte offset of the row, kOOB when the row is out of range
-  __device__ __forceinline__ void init(long ld, int mn0, int MN) {
+// One operand's share of the per-k-tile copy for this thread: NI wave
+// instructions (instruction g of the operand covers LDS bytes [1024 g, +1024)).
+template <int ROWS, bool KC, int NI>
+struct Copier {
+  uint32_t base[NI];  // byte offset at k = 0 (kOOB when the row / column is out of range)
+  int kk[NI];         // k offset of this lane's data within the k-tile
+  int gi[NI];         // instruction index within the operand tile
+  __device__ __forceinline__ void init(int wave, int nw, long ld, int mn0, int MN, int lane) {
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int idx = threadIdx.x + i * NT;
-      const int mn = mn0 + (idx >> 3);
-      row_off[i] = mn < MN ? (uint32_t)((long)mn * ld * 2) : kOOB;
-    }
-  }
-  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, int k0, int K) {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int idx = threadIdx.x + i * NT;
-      const int k = k0 + (idx & 7) * 8;
-      const uint32_t off = (k < K) ? row_off[i] + 2u * k : kOOB;
-      v[i] = bload(r, off | (row_off[i] & kOOB));
-    }
-  }
-  __device__ __forceinline__ void store(bf16* s) const {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int idx = threadIdx.x + i * NT;
-      *(uint4*)(s + lds_off(idx >> 3, idx & 7)) = v[i];
-    }
-  }
-};
-
-// Tile of ROWS rows (m or n) x 64 k from an mn-contiguous matrix: element
-// (r, k) at base[k * ld + r].  A thread owns one 8(k) x 8(mn) block; block b
-// goes to thread (b + SHIFT) % NT so that two such operands use disjoint
-// threads.
-template <int ROWS, int NT, int SHIFT>
-struct LoadMN {
-  static constexpr int NBLK = ROWS;  // (64 / 8) * (ROWS / 8)
-  static_assert(NBLK <= NT, "one 8x8 block per thread");
-  uint4 v[8];
-  int b;
-  uint32_t col_off;  // byte offset of the thread's 8 columns, kOOB when out of range
-  __device__ __forceinline__ void init(int mn0, int MN) {
-    b = ((int)threadIdx.x + NT - SHIFT) % NT;
-    const int mn = mn0 + (b % (ROWS / 8)) * 8;
-    col_off = (b < NBLK && mn < MN) ? (uint32_t)(2 * mn) : kOOB;
-  }
-  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, long ld, int k0, int K) {
-    if (b >= NBLK) return;
-    const int kb = b / (ROWS / 8);
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int k = k0 + kb * 8 + q;
-      const uint32_t off = (k < K) ? col_off + (uint32_t)((long)k * ld * 2) : kOOB;
-      v[q] = bload(r, off | (col_off & kOOB));
-    }
-  }
-  __device__ __forceinline__ void store(bf16* s) const {
-    if (b >= NBLK) return;
-    const int mb = b % (ROWS / 8), kb = b / (ROWS / 8);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      uint32_t o[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t x = comp(v[2 * q], j >> 1), y = comp(v[2 * q + 1], j >> 1);
-        o[q] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
+    for (int i = 0; i < NI; ++i) {
+      const int g = wave + nw * i;
+      gi[i] = g;
+      if (KC) {
+        const int row = 8 * g + (lane >> 3);
+        const int c = (lane & 7) ^ swz_k(row);
+        kk[i] = 8 * c;
+        base[i] = (mn0 + row < MN) ? (uint32_t)((long)(mn0 + row) * ld * 2) : kOOB;
+      } else {
+        constexpr int RPI = 512 / ROWS;  // k-rows per instruction
+        constexpr int CPR = ROWS / 8;    // chunks per k-row
+        const int krow = RPI * g + lane / CPR;
+        const int c = (lane % CPR) ^ swz_mn(krow);
+        kk[i] = krow;
+        base[i] = (mn0 + 8 * c < MN) ? (uint32_t)(2 * (mn0 + 8 * c)) : kOOB;
       }
-      *(uint4*)(s + lds_off(mb * 8 + j, kb)) = make_uint4(o[0], o[1], o[2], o[3]);
     }
   }
-};
-
-template <int ROWS, int NT, bool KC, int SHIFT> struct Operand;
-template <int ROWS, int NT, int SHIFT>
-struct Operand<ROWS, NT, true, SHIFT> : LoadK<ROWS, NT> {
-  __device__ __forceinline__ void init(long ld, int mn0, int MN) { LoadK<ROWS, NT>::init(ld, mn0, MN); }
-  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, long, int k0, int K) {
-    LoadK<ROWS, NT>::load(r, k0, K);
-  }
-};
-template <int ROWS, int NT, int SHIFT>
-struct Operand<ROWS, NT, false, SHIFT> : LoadMN<ROWS, NT, SHIFT> {
-  __device__ __forceinline__ void init(long, int mn0, int MN) { LoadMN<ROWS, NT, SHIFT>::init(mn0, MN); }
-};
-
-// 512-thread staging of a 256x64 A tile and a 256x64 B tile: threads
-// [0, 256) load A, [256, 512) load B, so each thread holds one set of eight
-// 16-byte vectors (k-contiguous: eight chunks; mn-contiguous: one 8x8 block).
-template <bool AK, bool BKC>
-struct SplitLoader {
-  uint4 v[8];
-  uint32_t off;   // k-contiguous: byte offset of row mn0 + lt/8; mn-contiguous: of column mn0 + 8 (lt%32)
-  int nvalid;     // k-contiguous: rows of this thread (lt/8 + 32 i) that are in range; else 0/1
-  int lt;
-  bool isA;
-  template <bool KC>
-  __device__ __forceinline__ void init_one(long ld, int mn0, int MN) {
-    if constexpr (KC) {
-      const int mn = mn0 + (lt >> 3);
-      off = (uint32_t)((long)mn * ld * 2);
-      nvalid = mn < MN ? (MN - mn + 31) / 32 : 0;
-    } else {
-      const int mn = mn0 + (lt & 31) * 8;
-      off = (uint32_t)(2 * mn);
-      nvalid = mn < MN ? 1 : 0;
-    }
-  }
-  __device__ __forceinline__ void init(const GemmParams& p, int m0, int n0) {
-    // wave-uniform role, so each branch keeps its buffer descriptor in SGPRs
-    isA = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < 4;
-    lt = threadIdx.x & 255;
-    if (isA) init_one<AK>(p.lda, m0, p.M);
-    else init_one<BKC>(p.ldb, n0, p.N);
-  }
-  template <bool KC>
-  __device__ __forceinline__ void load_one(__amdgpu_buffer_rsrc_t r, long ld, int k0, int K) {
-    if constexpr (KC) {
-      const int k = k0 + (lt & 7) * 8;
-      const uint32_t row_step = (uint32_t)(64 * ld);  // 32 rows, in bytes
-      const uint32_t base = off + 2u * k;
+  __device__ __forceinline__ void issue(const i32x4& r, char* tile, long ld, int k0, int K) const {
+    const uint32_t kstep = KC ? 2u : (uint32_t)(2 * ld);
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
-        v[i] = bload(r, (k < K && i < nvalid) ? base + i * row_step : kOOB);
-    } else {
-      const int kb = lt >> 5;
-      const uint32_t ld2 = (uint32_t)(2 * ld);
+    for (int i = 0; i < NI; ++i) {
+      const int k = k0 + kk[i];
+      const uint32_t off = (k < K && base[i] != kOOB) ? base[i] + (uint32_t)k * kstep : kOOB;
+      dma16(r, __builtin_amdgcn_readfirstlane(lds_addr(tile) + gi[i] * 1024), off);
+    }
+  }
+};
+
+// MFMA fragment (32 rows starting at r0 of the tile, k-step ks) of a staged operand.
+template <int ROWS, bool KC>
+__device__ __forceinline__ bf16x8 frag(const char* tile, int r0, int ks, int lane) {
+  if constexpr (KC) {
+    const int r = r0 + (lane & 31);
+    const int c = ks * 2 + (lane >> 5);
+    return *(const bf16x8*)(tile + r * 128 + ((c ^ swz_k(r)) << 4));
+  } else {
+    const int i = lane & 15;
+    const int mn = r0 + 16 * ((lane >> 4) & 1) + 4 * (i & 3);
+    const int k = 16 * ks + 8 * (lane >> 5) + (i >> 2);
+    const int c = mn >> 3;
+    const char* p0 = tile + k * (ROWS * 2) + ((c ^ swz_mn(k)) << 4) + 8 * (i & 1);
+    const char* p1 = p0 + 4 * (ROWS * 2);  // k + 4 keeps k % 4, hence the swizzle
+    s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p0);
+    s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p1);
+    s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8, v);
+  }
+}
+
+// MFMAs of one staged k-tile.  The fragments of k-step ks+1 are read while
+// the 8 MFMAs of k-step ks issue; scheduling groups pin that interleave
+// (one MFMA, then that k-step's share of LDS reads) so the reads stay ahead.
+template <int BM, int BN, bool AK, bool BKC>
+__device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][2], const char* ta, const char* tb, int wm,
+                                         int wn, int lane) {
+  constexpr int READS = 4 * (AK ? 1 : 2) + 2 * (BKC ? 1 : 2);  // LDS read instructions per k-step
+  constexpr int PER = (READS + 7) / 8;
+  bf16x8 af[2][4], bfr[2][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) af[0][i] = frag<BM, AK>(ta, wm * 128 + i * 32, 0, lane);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) bfr[0][j] = frag<BN, BKC>(tb, wn * 64 + j * 32, 0, lane);
+  __builtin_amdgcn_sched_group_barrier(0x100, READS, 0);
+#pragma unroll
+  for (int ks = 0; ks < BK / 16; ++ks) {
+    const int c = ks & 1;
+    if (ks + 1 < BK / 16) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[c ^ 1][i] = frag<BM, AK>(ta, wm * 128 + i * 32, ks + 1, lane);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) bfr[c ^ 1][j] = frag<BN, BKC>(tb, wn * 64 + j * 32, ks + 1, lane);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][i], bfr[c][j], acc[i][j], 0, 0, 0);
+    if (ks + 1 < BK / 16) {
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
-        const int k = k0 + kb * 8 + q;
-        v[q] = bload(r, (k < K && nvalid) ? off + (uint32_t)k * ld2 : kOOB);
-      }
-    }
-  }
-  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb, long lda,
-                                       long ldb, int k0, int K) {
-    if (isA) load_one<AK>(ra, lda, k0, K);
-    else load_one<BKC>(rb, ldb, k0, K);
-  }
-  template <bool KC>
-  __device__ __forceinline__ void store_one(bf16* s) const {
-    if constexpr (KC) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int idx = lt + i * 256;
-        *(uint4*)(s + lds_off(idx >> 3, idx & 7)) = v[i];
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, PER, 0);
       }
     } else {
-      const int mb = lt & 31, kb = lt >> 5;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        uint32_t o[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const uint32_t x = comp(v[2 * q], j >> 1), y = comp(v[2 * q + 1], j >> 1);
-          o[q] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
-        }
-        *(uint4*)(s + lds_off(mb * 8 + j, kb)) = make_uint4(o[0], o[1], o[2], o[3]);
-      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     }
   }
-  __device__ __forceinline__ void store(bf16* sa, bf16* sb) const {
-    if (isA) store_one<AK>(sa);
-    else store_one<BKC>(sb);
-  }
-};
+}
 
-template <int BM, int BN, int EPI>
+// vmcnt(0): this thread's copies have landed; the barrier then makes every
+// wave's copies visible and frees the stage just read for the next copy.
+__device__ __forceinline__ void stage_sync() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __syncthreads();
+}
+
+template <int EPI>
 __device__ __forceinline__ void epilogue(const GemmParams& p, f32x16 (&acc)[4][2], int m0, int n0,
-                                         int wm, int wn, int lane, long c_off) {
+                                         int lane, long c_off) {
   typedef typename EpiOut<EPI, bf16>::type OutT;
   OutT* C = (OutT*)p.C + c_off;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const int n = n0 + wn * 64 + j * 32 + (lane & 31);
+      const int n = n0 + j * 32 + (lane & 31);
       if (n >= p.N) continue;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int m = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int m = m0 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         if (m < p.M) epi_store<EPI, bf16>(p, (bf16*)C, m, n, acc[i][j][r]);
       }
     }
@@ -248,11 +204,19 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, f32x16 (&acc)[4][2
 template <int BM, int BN, bool AK, bool BKC, int EPI>
 __global__ __launch_bounds__((BM / 128) * (BN / 64) * 64) void gemm_bf16_kernel(GemmParams p) {
   constexpr int WN_ = BN / 64;
-  constexpr int NT = (BM / 128) * WN_ * 64;
-  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * BK];
-  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * BK];
+  constexpr int NW = (BM / 128) * WN_;
+  constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
+  constexpr int STAGE = A_BYTES + B_BYTES;
+  constexpr int NA = A_BYTES / 1024, NB = B_BYTES / 1024;  // wave instructions per k-tile
+  static_assert(NA % NW == 0 && NB % NW == 0, "copy split");
+  constexpr int NIA = NA / NW, NIB = NB / NW;
+  // Two stages as distinct LDS objects, so the compiler can tell that the
+  // copy into one stage does not alias the fragment reads from the other.
+  __shared__ __attribute__((aligned(1024))) char lds0[STAGE];
+  __shared__ __attribute__((aligned(1024))) char lds1[STAGE];
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / WN_, wn = wave % WN_;
 
   // Tile order: spread consecutive tiles over the 8 XCDs' own ranges, then
@@ -275,14 +239,18 @@ __global__ __launch_bounds__((BM / 128) * (BN / 64) * 64) void gemm_bf16_kernel(
   const bf16* A = (const bf16*)p.A + zb * p.a_bs + zh * p.a_hs;
   const bf16* B = (const bf16*)p.B + zb * p.b_bs + zh * p.b_hs;
   const long c_off = zb * p.c_bs + zh * p.c_hs;
-  // Extents of the operands (bytes from their base); rows beyond are zero.
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, 2L * (AK ? (long)p.M * p.lda : (long)p.K * p.lda));
-  const __amdgpu_buffer_rsrc_t rb = make_rsrc(B, 2L * (BKC ? (long)p.N * p.ldb : (long)p.K * p.ldb));
+  const i32x4 ra = make_rsrc(A, 2L * (AK ? (long)p.M * p.lda : (long)p.K * p.lda));
+  const i32x4 rb = make_rsrc(B, 2L * (BKC ? (long)p.N * p.ldb : (long)p.K * p.ldb));
 
   int kb = 0, ke = p.K;
   if (p.krange == KR_BELOW) ke = min(p.K, m0 + BM);
   else if (p.krange == KR_ABOVE) kb = (m0 / BK) * BK;
   const int nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
+
+  Copier<BM, AK, NIA> ca;
+  Copier<BN, BKC, NIB> cb;
+  ca.init(wave, NW, p.lda, m0, p.M, lane);
+  cb.init(wave, NW, p.ldb, n0, p.N, lane);
 
   f32x16 acc[4][2];
 #pragma unroll
@@ -292,68 +260,29 @@ __global__ __launch_bounds__((BM / 128) * (BN / 64) * 64) void gemm_bf16_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // Global -> register -> LDS staging of the k-tiles.
-  struct Pair {
-    Operand<BM, NT, AK, 0> a;
-    Operand<BN, NT, BKC, NT / 2> b;
-    __device__ __forceinline__ void init(const GemmParams& p, int m0, int n0) {
-      a.init(p.lda, m0, p.M);
-      b.init(p.ldb, n0, p.N);
-    }
-    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb, long lda,
-                                         long ldb, int k0, int K) {
-      a.load(ra, lda, k0, K);
-      b.load(rb, ldb, k0, K);
-    }
-    __device__ __forceinline__ void store(bf16* sa, bf16* sb) const {
-      a.store(sa);
-      b.store(sb);
-    }
-  };
-  typedef typename std::conditional<NT == 512 && BM == 256 && BN == 256, SplitLoader<AK, BKC>, Pair>::type Stager;
-  Stager ld;
-  ld.init(p, m0, n0);
+  // Tile t lives in stage t % 2.  The copy of tile t+1 is issued before the
+  // MFMAs of tile t.
   if (nk > 0) {
-    ld.load(ra, rb, p.lda, p.ldb, kb, ke);
-    ld.store(sA[0], sB[0]);
+    ca.issue(ra, lds0, p.lda, kb, ke);
+    cb.issue(rb, lds0 + A_BYTES, p.ldb, kb, ke);
   }
-  __syncthreads();
-
-  const int arow = wm * 128 + (lane & 31);
-  const int brow = wn * 64 + (lane & 31);
-  const int chalf = lane >> 5;
-  for (int t = 0; t < nk; ++t) {
-    const int cur = t & 1;
-    const bool more = t + 1 < nk;
-    if (more) ld.load(ra, rb, p.lda, p.ldb, kb + (t + 1) * BK, ke);
-    const bf16* a_s = sA[cur];
-    const bf16* b_s = sB[cur];
-    bf16x8 af[2][4], bfr[2][2];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) af[0][i] = *(const bf16x8*)(a_s + lds_off(arow + i * 32, chalf));
-#pragma unroll
-    for (int j = 0; j < 2; ++j) bfr[0][j] = *(const bf16x8*)(b_s + lds_off(brow + j * 32, chalf));
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int c = ks & 1;
-      if (ks + 1 < BK / 16) {
-        const int cn = (ks + 1) * 2 + chalf;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) af[c ^ 1][i] = *(const bf16x8*)(a_s + lds_off(arow + i * 32, cn));
-#pragma unroll
-        for (int j = 0; j < 2; ++j) bfr[c ^ 1][j] = *(const bf16x8*)(b_s + lds_off(brow + j * 32, cn));
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][i], bfr[c][j], acc[i][j], 0, 0, 0);
+  stage_sync();
+  int t = 0;
+  for (; t + 1 < nk; t += 2) {
+    ca.issue(ra, lds1, p.lda, kb + (t + 1) * BK, ke);
+    cb.issue(rb, lds1 + A_BYTES, p.ldb, kb + (t + 1) * BK, ke);
+    mma_tile<BM, BN, AK, BKC>(acc, lds0, lds0 + A_BYTES, wm, wn, lane);
+    stage_sync();
+    if (t + 2 < nk) {
+      ca.issue(ra, lds0, p.lda, kb + (t + 2) * BK, ke);
+      cb.issue(rb, lds0 + A_BYTES, p.ldb, kb + (t + 2) * BK, ke);
     }
-    if (more) ld.store(sA[cur ^ 1], sB[cur ^ 1]);
-    __syncthreads();
+    mma_tile<BM, BN, AK, BKC>(acc, lds1, lds1 + A_BYTES, wm, wn, lane);
+    stage_sync();
   }
+  if (t < nk) mma_tile<BM, BN, AK, BKC>(acc, lds0, lds0 + A_BYTES, wm, wn, lane);
 
-  epilogue<BM, BN, EPI>(p, acc, m0, n0, wm, wn, lane, c_off);
+  epilogue<EPI>(p, acc, m0 + wm * 128, n0 + wn * 64, lane, c_off);
 }
 
 template <bool AK, bool BKC, int EPI>
