@@ -13,16 +13,22 @@ template <class E> __device__ __forceinline__ E from_f32(float x);
 template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }  // round to nearest even
 
-// tanh form of GeLU: 0.5 u (1 + tanh(sqrt(2/pi) (u + 0.044715 u^3))).
-__device__ __forceinline__ float gelu_f(float u) {
+// tanh form of GeLU: 0.5 u (1 + tanh(z)), z = sqrt(2/pi) (u + 0.044715 u^3).
+// Evaluated through the identity 0.5 (1 + tanh z) = 1 / (1 + exp(-2 z)),
+// which needs one exponential and one reciprocal and has no cancellation.
+__device__ __forceinline__ float gelu_sig(float u) {
   const float c = 0.7978845608028654f;
-  return 0.5f * u * (1.0f + tanhf(c * (u + 0.044715f * u * u * u)));
+  const float z = c * (u + 0.044715f * u * u * u);
+  return 1.0f / (1.0f + __expf(-2.0f * z));
 }
 
+__device__ __forceinline__ float gelu_f(float u) { return u * gelu_sig(u); }
+
+// d/du gelu(u) = s + 2 u s (1 - s) z'(u), s = 0.5 (1 + tanh z).
 __device__ __forceinline__ float gelu_grad_f(float u) {
   const float c = 0.7978845608028654f;
-  float t = tanhf(c * (u + 0.044715f * u * u * u));
-  return 0.5f * (1.0f + t) + 0.5f * u * (1.0f - t * t) * c * (1.0f + 3.0f * 0.044715f * u * u);
+  const float s = gelu_sig(u);
+  return s + 2.0f * u * s * (1.0f - s) * c * (1.0f + 3.0f * 0.044715f * u * u);
 }
 
 __device__ __forceinline__ float wave_sum(float v) {

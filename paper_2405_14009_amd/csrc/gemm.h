@@ -78,6 +78,59 @@ __device__ __forceinline__ void epi_store(const GemmParams& p, E* C, int m, int 
   }
 }
 
+// Same epilogue on 4 consecutive columns n..n+3 (n % 4 == 0, all in range);
+// 8- or 16-byte vector accesses.
+template <int EPI, class E>
+__device__ __forceinline__ void epi_store4(const GemmParams& p, void* Cv, int m, int n, float4 v) {
+  const long i = (long)m * p.ldc + n;
+  auto ld4 = [](const E* q) -> float4 {
+    if constexpr (sizeof(E) == 2) {
+      const uint2 u = *(const uint2*)q;
+      return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                         __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+    } else {
+      return *(const float4*)q;
+    }
+  };
+  auto st4 = [](E* q, float4 f) {
+    if constexpr (sizeof(E) == 2) {
+      E t[4] = {from_f32<E>(f.x), from_f32<E>(f.y), from_f32<E>(f.z), from_f32<E>(f.w)};
+      *(uint2*)q = *(const uint2*)t;
+    } else {
+      *(float4*)q = f;
+    }
+  };
+  if constexpr (EPI == EPI_F32_ACC) {
+    float4* c = (float4*)((float*)Cv + i);
+    if (p.accumulate) {
+      const float4 o = *c;
+      v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+    }
+    *c = v;
+  } else if constexpr (EPI == EPI_F32_STORE) {
+    *(float4*)((float*)Cv + i) = v;
+  } else {
+    E* C = (E*)Cv;
+    if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RESID || EPI == EPI_BIAS_GELU) {
+      const float4 b = *(const float4*)(p.bias + n);
+      v.x += b.x; v.y += b.y; v.z += b.z; v.w += b.w;
+    }
+    if constexpr (EPI == EPI_BIAS_RESID) {
+      const float4 r = ld4((const E*)p.resid + (long)m * p.ld_resid + n);
+      v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
+    }
+    if constexpr (EPI == EPI_GELU_BWD) {
+      const float4 u = ld4((const E*)p.aux + (long)m * p.ld_aux + n);
+      v.x *= gelu_grad_f(u.x); v.y *= gelu_grad_f(u.y); v.z *= gelu_grad_f(u.z); v.w *= gelu_grad_f(u.w);
+    }
+    st4(C + i, v);
+    if constexpr (EPI == EPI_BIAS_GELU) {
+      st4((E*)p.C2 + (long)m * p.ldc2 + n,
+          make_float4(gelu_f(v.x), gelu_f(v.y), gelu_f(v.z), gelu_f(v.w)));
+    }
+  }
+}
+
 // Output element type of each epilogue given the activation type E.
 template <int EPI, class E>
 struct EpiOut { typedef E type; };

@@ -1,10 +1,12 @@
 // bf16 GEMM kernel template on CDNA4 matrix cores: v_mfma_f32_32x32x16_bf16,
 // fp32 accumulate.
 //
-// Tiles.  Each wave owns a 128 x 64 output tile (4 x 2 MFMA blocks of 32x32,
-// 128 accumulators); a BM x BN workgroup tile uses (BM/128) x (BN/64) waves:
-// 256x256 runs 8 waves (two per SIMD, hiding each other's latencies),
-// 256x128 runs 4.
+// Tiles.  A BM x BN workgroup tile runs 4 waves in a 2 x 2 grid (one per
+// SIMD); each wave owns a (BM/2) x (BN/2) tile of 32x32 MFMA blocks: 128 x 128
+// (256 fp32 accumulators) for 256x256 tiles, 128 x 64 for 256x128 tiles.
+// LDS bandwidth, not MFMA issue, bounds these kernels once operands are
+// staged through LDS, so the larger wave tile (8 fragment reads per 16 MFMAs
+// instead of 6 per 8) is the main lever.
 //
 // Staging.  k-tiles of 64 are copied from memory straight into LDS by
 // buffer-load-to-LDS instructions (each wave instruction deposits 64 lanes x
@@ -39,7 +41,9 @@ constexpr int BK = 64;
 constexpr uint32_t kOOB = 0x80000000u;  // buffer offset that is always out of range -> zeros
 
 // k-contiguous tiles: chunk c (8 elements) of row r lives at chunk c ^ swz_k(r).
-__device__ __forceinline__ int swz_k(int r) { return ((r >> 1) ^ (r >> 3)) & 7; }
+// Depends on r mod 32 only (so every 32-row MFMA block of a wave shares it)
+// and spreads any 8, and any 16, consecutive rows over distinct banks.
+__device__ __forceinline__ int swz_k(int r) { return (r & 7) ^ ((r >> 3) & 3); }
 // m/n-contiguous tiles: chunk c of k-row r lives at chunk c ^ swz_mn(r).
 __device__ __forceinline__ int swz_mn(int r) { return (r & 3) << 2; }
 
@@ -76,57 +80,85 @@ __device__ __forceinline__ uint32_t lds_addr(const char* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
 }
 
-// One operand's share of the per-k-tile copy for this thread: NI wave
-// instructions (instruction g of the operand covers LDS bytes [1024 g, +1024)).
+// One operand's share of the per-k-tile copy: this wave issues instructions
+// g = wave + 4 q (q < NI) of the operand's 1 KB slices.  Every slice of a wave
+// differs from its first by a fixed row (k-contiguous) or k-row
+// (m/n-contiguous) step, so two per-lane values describe all of them.
 template <int ROWS, bool KC, int NI>
 struct Copier {
-  uint32_t base[NI];  // byte offset at k = 0 (kOOB when the row / column is out of range)
-  int kk[NI];         // k offset of this lane's data within the k-tile
-  int gi[NI];         // instruction index within the operand tile
-  __device__ __forceinline__ void init(int wave, int nw, long ld, int mn0, int MN, int lane) {
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int g = wave + nw * i;
-      gi[i] = g;
-      if (KC) {
-        const int row = 8 * g + (lane >> 3);
-        const int c = (lane & 7) ^ swz_k(row);
-        kk[i] = 8 * c;
-        base[i] = (mn0 + row < MN) ? (uint32_t)((long)(mn0 + row) * ld * 2) : kOOB;
-      } else {
-        constexpr int RPI = 512 / ROWS;  // k-rows per instruction
-        constexpr int CPR = ROWS / 8;    // chunks per k-row
-        const int krow = RPI * g + lane / CPR;
-        const int c = (lane % CPR) ^ swz_mn(krow);
-        kk[i] = krow;
-        base[i] = (mn0 + 8 * c < MN) ? (uint32_t)(2 * (mn0 + 8 * c)) : kOOB;
-      }
+  uint32_t base;  // byte offset of this lane's row (k-contiguous) / column (m/n-contiguous) in slice 0
+  int kk;         // k offset of this lane's data within the k-tile, slice 0
+  int mn;         // this lane's row (k-contiguous) / first column (m/n-contiguous), slice 0
+  static constexpr int RPI = KC ? 8 : 512 / ROWS;  // rows (k-contiguous) or k-rows per slice
+  __device__ __forceinline__ void init(int wave, long ld, int mn0, int lane) {
+    if (KC) {
+      const int row = 8 * wave + (lane >> 3);
+      kk = 8 * ((lane & 7) ^ swz_k(row));  // the same for every slice: rows differ by 32 q
+      mn = mn0 + row;
+      base = (uint32_t)((long)mn * ld * 2);
+    } else {
+      constexpr int CPR = ROWS / 8;  // chunks per k-row
+      const int krow = RPI * wave + lane / CPR;
+      const int c = (lane % CPR) ^ swz_mn(krow);  // k-rows of later slices differ by a multiple of 4
+      kk = krow;
+      mn = mn0 + 8 * c;
+      base = (uint32_t)(2 * mn);
     }
   }
-  __device__ __forceinline__ void issue(const i32x4& r, char* tile, long ld, int k0, int K) const {
-    const uint32_t kstep = KC ? 2u : (uint32_t)(2 * ld);
+  __device__ __forceinline__ void issue(const i32x4& r, char* tile, int wave, long ld, int MN, int k0,
+                                        int K) const {
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int k = k0 + kk[i];
-      const uint32_t off = (k < K && base[i] != kOOB) ? base[i] + (uint32_t)k * kstep : kOOB;
-      dma16(r, __builtin_amdgcn_readfirstlane(lds_addr(tile) + gi[i] * 1024), off);
+    for (int q = 0; q < NI; ++q) {
+      uint32_t off;
+      if (KC) {
+        const int k = k0 + kk;
+        const bool ok = (mn + 32 * q < MN) && (k < K);
+        off = ok ? base + (uint32_t)(32 * q) * (uint32_t)(2 * ld) + 2u * k : kOOB;
+      } else {
+        const int k = k0 + kk + 4 * RPI * q;
+        off = (mn < MN && k < K) ? base + (uint32_t)k * (uint32_t)(2 * ld) : kOOB;
+      }
+      dma16(r, __builtin_amdgcn_readfirstlane(lds_addr(tile) + (wave + 4 * q) * 1024), off);
     }
   }
 };
 
-// MFMA fragment (32 rows starting at r0 of the tile, k-step ks) of a staged operand.
-template <int ROWS, bool KC>
-__device__ __forceinline__ bf16x8 frag(const char* tile, int r0, int ks, int lane) {
+// Per-lane byte offsets of a wave's MFMA fragments in a staged operand tile.
+// k-contiguous: off[ks] for k-step ks (block i of 32 rows adds 4096 i).
+// m/n-contiguous: off[b] for 32-row block b (k-step ks adds 32 ks rows of
+// the tile, the second half-read 4 k-rows).
+template <int ROWS, bool KC, int NBLK>
+struct FragOffsets {
+  static constexpr int N = KC ? 4 : NBLK;
+  uint32_t off[N];
+  __device__ __forceinline__ void init(int r0, int lane) {
+    if constexpr (KC) {
+      const int r = r0 + (lane & 31);
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int c = ks * 2 + (lane >> 5);
+        off[ks] = (uint32_t)(r * 128 + ((c ^ swz_k(r)) << 4));
+      }
+    } else {
+      const int i = lane & 15;
+      const int k = 8 * (lane >> 5) + (i >> 2);
+#pragma unroll
+      for (int b = 0; b < NBLK; ++b) {
+        const int mn = r0 + 32 * b + 16 * ((lane >> 4) & 1) + 4 * (i & 3);
+        off[b] = (uint32_t)(k * (ROWS * 2) + (((mn >> 3) ^ swz_mn(k)) << 4) + 8 * (i & 1));
+      }
+    }
+  }
+};
+
+// Fragment of 32-row block b, k-step ks: 8 k-consecutive values of one row per lane.
+template <int ROWS, bool KC, int NBLK>
+__device__ __forceinline__ bf16x8 frag(const char* tile, const FragOffsets<ROWS, KC, NBLK>& fo, int b,
+                                       int ks) {
   if constexpr (KC) {
-    const int r = r0 + (lane & 31);
-    const int c = ks * 2 + (lane >> 5);
-    return *(const bf16x8*)(tile + r * 128 + ((c ^ swz_k(r)) << 4));
+    return *(const bf16x8*)(tile + fo.off[ks] + 4096 * b);
   } else {
-    const int i = lane & 15;
-    const int mn = r0 + 16 * ((lane >> 4) & 1) + 4 * (i & 3);
-    const int k = 16 * ks + 8 * (lane >> 5) + (i >> 2);
-    const int c = mn >> 3;
-    const char* p0 = tile + k * (ROWS * 2) + ((c ^ swz_mn(k)) << 4) + 8 * (i & 1);
+    const char* p0 = tile + fo.off[b] + 16 * ks * (ROWS * 2);
     const char* p1 = p0 + 4 * (ROWS * 2);  // k + 4 keeps k % 4, hence the swizzle
     s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p0);
     s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p1);
@@ -135,42 +167,45 @@ __device__ __forceinline__ bf16x8 frag(const char* tile, int r0, int ks, int lan
   }
 }
 
-// MFMAs of one staged k-tile.  The fragments of k-step ks+1 are read while
-// the 8 MFMAs of k-step ks issue; scheduling groups pin that interleave
-// (one MFMA, then that k-step's share of LDS reads) so the reads stay ahead.
-template <int BM, int BN, bool AK, bool BKC>
-__device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][2], const char* ta, const char* tb, int wm,
-                                         int wn, int lane) {
-  constexpr int READS = 4 * (AK ? 1 : 2) + 2 * (BKC ? 1 : 2);  // LDS read instructions per k-step
-  constexpr int PER = (READS + 7) / 8;
-  bf16x8 af[2][4], bfr[2][2];
+// MFMAs of one staged k-tile for a wave tile of 4 x TN blocks of 32x32.  The
+// fragments of k-step ks+1 are read while the MFMAs of k-step ks issue;
+// scheduling groups pin that interleave (one MFMA, then that k-step's share
+// of LDS reads) so the reads stay ahead of their use.
+template <int BM, int BN, bool AK, bool BKC, int TN>
+__device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][TN], const char* ta, const char* tb,
+                                         const FragOffsets<BM, AK, 4>& fa,
+                                         const FragOffsets<BN, BKC, TN>& fb) {
+  constexpr int READS = 4 * (AK ? 1 : 2) + TN * (BKC ? 1 : 2);  // LDS read instructions per k-step
+  constexpr int NMFMA = 4 * TN;
+  constexpr int PER = (READS + NMFMA - 1) / NMFMA;
+  bf16x8 af[2][4], bfr[2][TN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) af[0][i] = frag<BM, AK>(ta, wm * 128 + i * 32, 0, lane);
+  for (int i = 0; i < 4; ++i) af[0][i] = frag(ta, fa, i, 0);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) bfr[0][j] = frag<BN, BKC>(tb, wn * 64 + j * 32, 0, lane);
+  for (int j = 0; j < TN; ++j) bfr[0][j] = frag(tb, fb, j, 0);
   __builtin_amdgcn_sched_group_barrier(0x100, READS, 0);
 #pragma unroll
   for (int ks = 0; ks < BK / 16; ++ks) {
     const int c = ks & 1;
     if (ks + 1 < BK / 16) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) af[c ^ 1][i] = frag<BM, AK>(ta, wm * 128 + i * 32, ks + 1, lane);
+      for (int i = 0; i < 4; ++i) af[c ^ 1][i] = frag(ta, fa, i, ks + 1);
 #pragma unroll
-      for (int j = 0; j < 2; ++j) bfr[c ^ 1][j] = frag<BN, BKC>(tb, wn * 64 + j * 32, ks + 1, lane);
+      for (int j = 0; j < TN; ++j) bfr[c ^ 1][j] = frag(tb, fb, j, ks + 1);
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < TN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][i], bfr[c][j], acc[i][j], 0, 0, 0);
     if (ks + 1 < BK / 16) {
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
+      for (int q = 0; q < NMFMA; ++q) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, PER, 0);
       }
     } else {
-      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, NMFMA, 0);
     }
   }
 }
@@ -182,29 +217,43 @@ __device__ __forceinline__ void stage_sync() {
   __syncthreads();
 }
 
-template <int EPI>
-__device__ __forceinline__ void epilogue(const GemmParams& p, f32x16 (&acc)[4][2], int m0, int n0,
-                                         int lane, long c_off) {
+// Epilogue through LDS.  For each 32-row block-row of its tile a wave writes
+// its accumulators (MFMA layout: lane l holds column l % 32, rows
+// 8 (r / 4) + 4 (l / 32) + r % 4) to a row-major fp32 LDS tile (rows padded by
+// 8 floats so the two half-waves hit disjoint banks), then re-reads it row by
+// row so each lane applies the epilogue to 4 consecutive columns with vector
+// global accesses.  `sm` is this wave's private LDS region.
+template <int EPI, int TN>
+__device__ __forceinline__ void epilogue(const GemmParams& p, f32x16 (&acc)[4][TN], float* sm, int m0,
+                                         int n0, int lane, long c_off) {
+  constexpr int COLS = 32 * TN, STRIDE = COLS + 8;
   typedef typename EpiOut<EPI, bf16>::type OutT;
-  OutT* C = (OutT*)p.C + c_off;
+  void* C = (OutT*)p.C + c_off;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 4; ++i) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int n = n0 + j * 32 + (lane & 31);
-      if (n >= p.N) continue;
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = m0 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (m < p.M) epi_store<EPI, bf16>(p, (bf16*)C, m, n, acc[i][j][r]);
-      }
+      for (int r = 0; r < 16; ++r)
+        sm[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * STRIDE + 32 * j + (lane & 31)] = acc[i][j][r];
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll 2
+    for (int q = 0; q < COLS / 8; ++q) {
+      const int idx = lane + 64 * q;
+      const int row = idx / (COLS / 4), c4 = idx % (COLS / 4);
+      const float4 v = *(const float4*)(sm + row * STRIDE + 4 * c4);
+      const int m = m0 + i * 32 + row, n = n0 + 4 * c4;
+      if (m < p.M && n < p.N) epi_store4<EPI, bf16>(p, C, m, n, v);
     }
+    __builtin_amdgcn_wave_barrier();
+  }
 }
 
 template <int BM, int BN, bool AK, bool BKC, int EPI>
-__global__ __launch_bounds__((BM / 128) * (BN / 64) * 64) void gemm_bf16_kernel(GemmParams p) {
-  constexpr int WN_ = BN / 64;
-  constexpr int NW = (BM / 128) * WN_;
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
+  static_assert(BM == 256 && (BN == 256 || BN == 128), "tile shapes");
+  constexpr int WN_ = 2, NW = 4;
+  constexpr int TN = BN / 64;  // 32-wide blocks per wave along n
   constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
   constexpr int STAGE = A_BYTES + B_BYTES;
   constexpr int NA = A_BYTES / 1024, NB = B_BYTES / 1024;  // wave instructions per k-tile
@@ -249,40 +298,49 @@ __global__ __launch_bounds__((BM / 128) * (BN / 64) * 64) void gemm_bf16_kernel(
 
   Copier<BM, AK, NIA> ca;
   Copier<BN, BKC, NIB> cb;
-  ca.init(wave, NW, p.lda, m0, p.M, lane);
-  cb.init(wave, NW, p.ldb, n0, p.N, lane);
+  ca.init(wave, p.lda, m0, lane);
+  cb.init(wave, p.ldb, n0, lane);
+  FragOffsets<BM, AK, 4> fa;
+  FragOffsets<BN, BKC, TN> fb;
+  fa.init(wm * 128, lane);
+  fb.init(wn * (BN / 2), lane);
 
-  f32x16 acc[4][2];
+  f32x16 acc[4][TN];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   // Tile t lives in stage t % 2.  The copy of tile t+1 is issued before the
   // MFMAs of tile t.
   if (nk > 0) {
-    ca.issue(ra, lds0, p.lda, kb, ke);
-    cb.issue(rb, lds0 + A_BYTES, p.ldb, kb, ke);
+    ca.issue(ra, lds0, wave, p.lda, p.M, kb, ke);
+    cb.issue(rb, lds0 + A_BYTES, wave, p.ldb, p.N, kb, ke);
   }
   stage_sync();
   int t = 0;
   for (; t + 1 < nk; t += 2) {
-    ca.issue(ra, lds1, p.lda, kb + (t + 1) * BK, ke);
-    cb.issue(rb, lds1 + A_BYTES, p.ldb, kb + (t + 1) * BK, ke);
-    mma_tile<BM, BN, AK, BKC>(acc, lds0, lds0 + A_BYTES, wm, wn, lane);
+    ca.issue(ra, lds1, wave, p.lda, p.M, kb + (t + 1) * BK, ke);
+    cb.issue(rb, lds1 + A_BYTES, wave, p.ldb, p.N, kb + (t + 1) * BK, ke);
+    mma_tile<BM, BN, AK, BKC, TN>(acc, lds0, lds0 + A_BYTES, fa, fb);
     stage_sync();
     if (t + 2 < nk) {
-      ca.issue(ra, lds0, p.lda, kb + (t + 2) * BK, ke);
-      cb.issue(rb, lds0 + A_BYTES, p.ldb, kb + (t + 2) * BK, ke);
+      ca.issue(ra, lds0, wave, p.lda, p.M, kb + (t + 2) * BK, ke);
+      cb.issue(rb, lds0 + A_BYTES, wave, p.ldb, p.N, kb + (t + 2) * BK, ke);
     }
-    mma_tile<BM, BN, AK, BKC>(acc, lds1, lds1 + A_BYTES, wm, wn, lane);
+    mma_tile<BM, BN, AK, BKC, TN>(acc, lds1, lds1 + A_BYTES, fa, fb);
     stage_sync();
   }
-  if (t < nk) mma_tile<BM, BN, AK, BKC>(acc, lds0, lds0 + A_BYTES, wm, wn, lane);
+  if (t < nk) mma_tile<BM, BN, AK, BKC, TN>(acc, lds0, lds0 + A_BYTES, fa, fb);
 
-  epilogue<EPI>(p, acc, m0 + wm * 128, n0 + wn * 64, lane, c_off);
+  // LDS is free once every wave is past its last k-tile.
+  __syncthreads();
+  constexpr int EPI_BYTES = 32 * (32 * TN + 8) * 4;  // one wave's block-row tile
+  static_assert(2 * EPI_BYTES <= STAGE, "epilogue tiles fit two per stage");
+  float* sm = (float*)((wave < 2 ? lds0 : lds1) + (wave & 1) * EPI_BYTES);
+  epilogue<EPI, TN>(p, acc, sm, m0 + wm * 128, n0 + wn * (BN / 2), lane, c_off);
 }
 
 template <bool AK, bool BKC, int EPI>
@@ -300,7 +358,7 @@ hipError_t launch_bf16(const GemmParams& p, hipStream_t s) {
     hipLaunchKernelGGL((gemm_bf16_kernel<256, 128, AK, BKC, EPI>), dim3(tiles, z), dim3(256), 0, s, p);
   } else {
     const int tiles = ((p.M + 255) / 256) * ((p.N + 255) / 256);
-    hipLaunchKernelGGL((gemm_bf16_kernel<256, 256, AK, BKC, EPI>), dim3(tiles, z), dim3(512), 0, s, p);
+    hipLaunchKernelGGL((gemm_bf16_kernel<256, 256, AK, BKC, EPI>), dim3(tiles, z), dim3(256), 0, s, p);
   }
   return hipGetLastError();
 }
