@@ -77,6 +77,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="gpt6.7b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--single-w", action="store_true",
+                    help="one weight-pass call per micro-batch instead of merging consecutive "
+                         "weight passes of the op list into one batched call")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the per-kernel events (for external profilers)")
     args = ap.parse_args()
@@ -113,23 +116,36 @@ def main() -> int:
     log(f"setup {time.perf_counter() - t:.1f} s (stage arenas "
         f"{(stage.state_bytes + stage.stash_bytes + stage.work_bytes) / 2**30:.1f} GiB)")
 
+    # Deferred weight passes that follow each other in the op list run as one
+    # batched call (same gradients and op-log records as one call each).
+    steps_ops = []
+    for op in ops:
+        if (op.kind == "W" and not args.single_w and steps_ops and steps_ops[-1][0] == "W"
+                and len(steps_ops[-1][1]) < 32):
+            steps_ops[-1][1].append(op.mb)
+        else:
+            steps_ops.append((op.kind, [op.mb]))
+
     def run_step(events=None):
-        for op in ops:
+        for kind, mbs in steps_ops:
             if events is not None:
                 a = torch.cuda.Event(enable_timing=True)
                 a.record()
-            if op.kind == "F":
-                stage.forward(op.mb, xs[tuple(op.mb)], ys[tuple(op.mb)])
-            elif op.kind == "B":
-                stage.backward_input(op.mb, dys[tuple(op.mb)], dxs[tuple(op.mb)])
-            elif op.kind == "W":
-                stage.backward_weight(op.mb)
+            if kind == "F":
+                stage.forward(mbs[0], xs[tuple(mbs[0])], ys[tuple(mbs[0])])
+            elif kind == "B":
+                stage.backward_input(mbs[0], dys[tuple(mbs[0])], dxs[tuple(mbs[0])])
+            elif kind == "W":
+                if len(mbs) == 1:
+                    stage.backward_weight(mbs[0])
+                else:
+                    stage.backward_weight_many(mbs)
             else:
                 stage.optimizer_step()
             if events is not None:
                 b = torch.cuda.Event(enable_timing=True)
                 b.record()
-                events.append((op.kind, a, b))
+                events.append((kind, a, b))
 
     for i in range(args.warmup):
         run_step()
@@ -168,7 +184,8 @@ def main() -> int:
         "config": {"workload": workload_name(cfg), "layers": cfg.layers, "hidden": cfg.hidden,
                    "heads": cfg.heads, "ffn": cfg.ffn, "seq_len": cfg.seq,
                    "micro_batch": cfg.micro_batch, "micro_batches": cfg.n_mb,
-                   "tokens_per_micro_batch": cfg.tokens, "parallelism": "one stage, one GPU"},
+                   "tokens_per_micro_batch": cfg.tokens, "parallelism": "one stage, one GPU",
+                   "weight_pass_calls_per_step": sum(1 for k, _ in steps_ops if k == "W")},
         "mb_per_s": round(cfg.n_mb * args.steps / wall, 2),
         "pct_bf16_peak": round(100 * it_flops * args.steps / wall / 1e12 / PEAK_BF16_TFLOPS, 2),
     }

@@ -182,6 +182,20 @@ rc_status rc_stage_backward_input(rc_stage* st, rc_mb mb, const void* dy, void* 
  * Errors: RC_ERR_BAD_STATE (mb has not run B, or already ran W), RC_ERR_HIP. */
 rc_status rc_stage_backward_weight(rc_stage* st, rc_mb mb);
 
+/* B_weight of n micro-batches mbs[0..n) at once (the weight pass may be
+ * deferred and run in any order and grouping, Sec. 3.2; gradients are sums
+ * over micro-batches, Eq. 1).  Same result and op-log records as n
+ * consecutive rc_stage_backward_weight calls in the given order (fp32 sums
+ * in another association order), but each linear's gradient is one product
+ * over the n micro-batches' concatenated tokens and each bias / LayerNorm
+ * parameter one reduction, so a pass over several deferred micro-batches runs
+ * longer, fuller kernels.  mbs: host array of n distinct micro-batches,
+ * 1 <= n <= 32; all-or-nothing: no state changes on error.
+ * Errors: RC_ERR_INVALID_ARG (n out of range, mbs NULL),
+ *         RC_ERR_BAD_STATE (a micro-batch has not run B, already ran W, or is
+ *         listed twice), RC_ERR_HIP. */
+rc_status rc_stage_backward_weight_many(rc_stage* st, const rc_mb* mbs, int32_t n);
+
 /* AdamW over every parameter of the stage with g = grad_scale * gradient;
  * refreshes the bf16 weight copies; closes the iteration (every micro-batch
  * state is reset, the iteration counter advances).  With no weight pass in

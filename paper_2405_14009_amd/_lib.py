@@ -21,7 +21,8 @@ RC_NUM_PARAMS = 12
 EXPORTED = (
     "rc_stage_memory_requirements", "rc_stage_create", "rc_stage_destroy", "rc_stage_load_param",
     "rc_stage_read", "rc_stage_forward", "rc_stage_backward_input", "rc_stage_backward_weight",
-    "rc_stage_optimizer_step", "rc_stage_op_log", "rc_stage_stash_usage", "rc_stage_set_stream",
+    "rc_stage_backward_weight_many", "rc_stage_optimizer_step", "rc_stage_op_log",
+    "rc_stage_stash_usage", "rc_stage_set_stream",
     "rc_stage_synchronize", "rc_stage_profile_enable", "rc_stage_profile_read", "rc_last_error",
 )
 
@@ -101,6 +102,7 @@ def load() -> ctypes.CDLL:
         "rc_stage_forward": [P, RcMb, P, P],
         "rc_stage_backward_input": [P, RcMb, P, P],
         "rc_stage_backward_weight": [P, RcMb],
+        "rc_stage_backward_weight_many": [P, ctypes.POINTER(RcMb), I32],
         "rc_stage_optimizer_step": [P, F32],
         "rc_stage_op_log": [P, ctypes.POINTER(RcOpRecord), I32, ctypes.POINTER(I32)],
         "rc_stage_stash_usage": [P, ctypes.POINTER(I32), ctypes.POINTER(I32)],

@@ -31,6 +31,8 @@ enum KRange {
   KR_ABOVE = 2   // k >= m0 rounded down: operand A is zero for k < m (transposed causal P, dS)
 };
 
+constexpr int GEMM_MAX_SEG = 32;
+
 struct GemmParams {
   int M, N, K;
   const void* A; long lda; int a_kcontig;
@@ -46,6 +48,14 @@ struct GemmParams {
   const void* aux; long ld_aux;
   void* C2; long ldc2;
   int accumulate;
+  // Reduction split into segments of kseg_len (0: one segment).  Segment s
+  // of A / B starts at segA[s] / segB[s] (A, B are ignored); within a segment
+  // the layouts above apply with k counted from the segment start.  Used to
+  // run several micro-batches' weight gradients as one product over their
+  // concatenated tokens.
+  int kseg_len;
+  const void* segA[GEMM_MAX_SEG];
+  const void* segB[GEMM_MAX_SEG];
 };
 
 // Shapes must satisfy: M, N, K multiples of 8 when an operand is loaded

@@ -314,22 +314,30 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   // Tile t lives in stage t % 2.  The copy of tile t+1 is issued before the
-  // MFMAs of tile t.
-  if (nk > 0) {
-    ca.issue(ra, lds0, wave, p.lda, p.M, kb, ke);
-    cb.issue(rb, lds0 + A_BYTES, wave, p.ldb, p.N, kb, ke);
-  }
+  // MFMAs of tile t.  With a segmented reduction the k-tile's segment selects
+  // the operand bases (a k-tile never straddles segments).
+  auto issue = [&](char* st, int k0) {
+    if (p.kseg_len > 0) {
+      const int sg = k0 / p.kseg_len, kin = k0 - sg * p.kseg_len;
+      const i32x4 sa = make_rsrc((const bf16*)p.segA[sg] + zb * p.a_bs + zh * p.a_hs,
+                                 2L * (AK ? (long)p.M * p.lda : (long)p.kseg_len * p.lda));
+      const i32x4 sb = make_rsrc((const bf16*)p.segB[sg] + zb * p.b_bs + zh * p.b_hs,
+                                 2L * (BKC ? (long)p.N * p.ldb : (long)p.kseg_len * p.ldb));
+      ca.issue(sa, st, wave, p.lda, p.M, kin, p.kseg_len);
+      cb.issue(sb, st + A_BYTES, wave, p.ldb, p.N, kin, p.kseg_len);
+    } else {
+      ca.issue(ra, st, wave, p.lda, p.M, k0, ke);
+      cb.issue(rb, st + A_BYTES, wave, p.ldb, p.N, k0, ke);
+    }
+  };
+  if (nk > 0) issue(lds0, kb);
   stage_sync();
   int t = 0;
   for (; t + 1 < nk; t += 2) {
-    ca.issue(ra, lds1, wave, p.lda, p.M, kb + (t + 1) * BK, ke);
-    cb.issue(rb, lds1 + A_BYTES, wave, p.ldb, p.N, kb + (t + 1) * BK, ke);
+    issue(lds1, kb + (t + 1) * BK);
     mma_tile<BM, BN, AK, BKC, TN>(acc, lds0, lds0 + A_BYTES, fa, fb);
     stage_sync();
-    if (t + 2 < nk) {
-      ca.issue(ra, lds0, wave, p.lda, p.M, kb + (t + 2) * BK, ke);
-      cb.issue(rb, lds0 + A_BYTES, wave, p.ldb, p.N, kb + (t + 2) * BK, ke);
-    }
+    if (t + 2 < nk) issue(lds0, kb + (t + 2) * BK);
     mma_tile<BM, BN, AK, BKC, TN>(acc, lds1, lds1 + A_BYTES, fa, fb);
     stage_sync();
   }

@@ -17,6 +17,10 @@ static hipError_t gemm_bf16_nn(const GemmParams& p, hipStream_t s) {
 
 hipError_t gemm_bf16(const GemmParams& p, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0 || p.batch * p.heads <= 0) return hipSuccess;
+  // a segmented reduction needs whole 64-deep k-tiles per segment
+  if (p.kseg_len > 0 && (p.kseg_len % 64 || p.K % p.kseg_len || p.K / p.kseg_len > GEMM_MAX_SEG ||
+                         p.krange != KR_FULL))
+    return hipErrorInvalidValue;
   if (p.a_kcontig && !p.b_kcontig) return gemm_bf16_nn(p, s);
   if (p.a_kcontig && p.b_kcontig) return gemm_bf16_nt(p, s);
   if (!p.a_kcontig && !p.b_kcontig) return gemm_bf16_tn(p, s);

@@ -33,13 +33,29 @@ __global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmParams p) {
       if (AK) { mm = e / TK; kk = e % TK; } else { kk = e / TB; mm = e % TB; }
       const int m = m0 + mm, k = k0 + kk;
       float va = 0.f;
-      if (m < p.M && k < ke) va = AK ? A[(long)m * p.lda + k] : A[(long)k * p.lda + m];
+      if (m < p.M && k < ke) {
+        const float* a = A;
+        int kl = k;
+        if (p.kseg_len > 0) {
+          a = (const float*)p.segA[k / p.kseg_len] + zb * p.a_bs + zh * p.a_hs;
+          kl = k % p.kseg_len;
+        }
+        va = AK ? a[(long)m * p.lda + kl] : a[(long)kl * p.lda + m];
+      }
       sA[kk][mm] = va;
       int nn;
       if (BKC) { nn = e / TK; kk = e % TK; } else { kk = e / TB; nn = e % TB; }
       const int n = n0 + nn, k2 = k0 + kk;
       float vb = 0.f;
-      if (n < p.N && k2 < ke) vb = BKC ? B[(long)n * p.ldb + k2] : B[(long)k2 * p.ldb + n];
+      if (n < p.N && k2 < ke) {
+        const float* b = B;
+        int kl = k2;
+        if (p.kseg_len > 0) {
+          b = (const float*)p.segB[k2 / p.kseg_len] + zb * p.b_bs + zh * p.b_hs;
+          kl = k2 % p.kseg_len;
+        }
+        vb = BKC ? b[(long)n * p.ldb + kl] : b[(long)kl * p.ldb + n];
+      }
       sB[kk][nn] = vb;
     }
     __syncthreads();
@@ -86,6 +102,7 @@ hipError_t launch_epi(const GemmParams& p, hipStream_t s) {
 
 hipError_t gemm_f32(const GemmParams& p, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0 || p.batch * p.heads <= 0) return hipSuccess;
+  if (p.kseg_len > 0 && (p.K % p.kseg_len || p.K / p.kseg_len > GEMM_MAX_SEG)) return hipErrorInvalidValue;
   if (p.a_kcontig && !p.b_kcontig) return launch_epi<true, false>(p, s);
   if (p.a_kcontig && p.b_kcontig) return launch_epi<true, true>(p, s);
   if (!p.a_kcontig && !p.b_kcontig) return launch_epi<false, false>(p, s);

@@ -15,17 +15,23 @@ hipError_t ln_backward(int elt, const void* dout, const void* x, const float* me
                        const float* rstd, const float* g, const void* resid, void* dx, long rows,
                        int h, hipStream_t s);
 
-// Column reductions over rows of a [rows, n] matrix with leading dimension ld,
-// into fp32 outputs (overwrite or accumulate), deterministic two-stage:
-//   bias:  db[c] (+)= sum_r dout[r, c]
-//   ln:    dg[c] (+)= sum_r dout[r, c] * (x[r, c] - mean[r]) * rstd[r];  db as above
-// part must hold 2 * ceil(rows / 64) * n floats.
-hipError_t colsum_bias(int elt, const void* dout, long ld, long rows, int n, float* db,
-                       int accumulate, float* part, hipStream_t s);
-hipError_t colsum_ln(int elt, const void* dout, const void* x, const float* mean,
-                     const float* rstd, long rows, int n, float* dg, float* db, int accumulate,
-                     float* part, hipStream_t s);
-long colsum_part_floats(long rows, int n);
+// Column reductions over the rows of nseg segments (one per micro-batch) of
+// a [rows, n] matrix with leading dimension ld, into fp32 outputs (overwrite
+// or accumulate); deterministic two-stage sums (64-row partials, then a fixed
+// order).  n % 4 == 0.
+//   bias (ln = false):  db[c] (+)= sum_r dout[r, c]
+//   ln   (ln = true):   dg[c] (+)= sum_r dout[r, c] * (x[r, c] - mean[r]) * rstd[r];  db as above
+// (x has leading dimension n).  part must hold colsum_part_floats(rows, n, nseg) floats.
+constexpr int COLSUM_MAX_SEG = 32;
+struct ColSegs {
+  const void* dout[COLSUM_MAX_SEG];
+  const void* x[COLSUM_MAX_SEG];
+  const float* mean[COLSUM_MAX_SEG];
+  const float* rstd[COLSUM_MAX_SEG];
+};
+hipError_t colsum(int elt, bool ln, const ColSegs& segs, int nseg, long ld, long rows, int n, float* dg,
+                  float* db, int accumulate, float* part, hipStream_t s);
+long colsum_part_floats(long rows, int n, int nseg);
 
 // Attention softmax over materialised scores, rows of length s, z*s rows.
 //   forward:  P[r, c] = exp(scale S[r, c] - max) / sum  for c <= q (causal) else 0

@@ -9,6 +9,13 @@ namespace {
 constexpr int NT = 256;
 constexpr int CHUNK = 64;  // rows per partial sum of the column reductions
 
+__device__ __forceinline__ float4 load4(const float* p) { return *(const float4*)p; }
+__device__ __forceinline__ float4 load4(const bf16* p) {
+  const uint2 u = *(const uint2*)p;
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                     __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+}
+
 template <class E>
 __global__ __launch_bounds__(NT) void ln_fwd_k(const E* __restrict__ x, const float* __restrict__ g,
                                                const float* __restrict__ b, E* __restrict__ y,
@@ -64,34 +71,54 @@ __global__ __launch_bounds__(NT) void ln_bwd_k(const E* __restrict__ dout, const
   }
 }
 
+// Column sums over the rows of nseg segments (one per micro-batch) of a
+// [rows, n] matrix: chunk y of 64 rows of segment y / cps writes its partial
+// sums of 4 consecutive columns per thread to part[y][n].
 template <class E, bool LN>
-__global__ __launch_bounds__(NT) void colsum_part_k(const E* __restrict__ dout, long ld,
-                                                    const E* __restrict__ x,
-                                                    const float* __restrict__ mean,
-                                                    const float* __restrict__ rstd, long rows,
-                                                    int n, float* __restrict__ part_b,
+__global__ __launch_bounds__(NT) void colsum_part_k(ColSegs sg, long ld, long rows, int n, int cps,
+                                                    float* __restrict__ part_b,
                                                     float* __restrict__ part_g) {
-  const int c = blockIdx.x * NT + threadIdx.x;
+  const int c = 4 * (blockIdx.x * NT + threadIdx.x);
   if (c >= n) return;
-  const long r0 = (long)blockIdx.y * CHUNK;
+  const int seg = blockIdx.y / cps, ch = blockIdx.y % cps;
+  const E* dout = (const E*)sg.dout[seg];
+  const E* x = (const E*)sg.x[seg];
+  const float* mean = sg.mean[seg];
+  const float* rstd = sg.rstd[seg];
+  const long r0 = (long)ch * CHUNK;
   const long r1 = min(rows, r0 + CHUNK);
-  float sb = 0.f, sg = 0.f;
+  float4 sb = make_float4(0.f, 0.f, 0.f, 0.f), sgm = sb;
   for (long r = r0; r < r1; ++r) {
-    const float d = to_f32(dout[r * ld + c]);
-    sb += d;
-    if (LN) sg += d * (to_f32(x[r * n + c]) - mean[r]) * rstd[r];
+    const float4 d = load4(dout + r * ld + c);
+    sb.x += d.x; sb.y += d.y; sb.z += d.z; sb.w += d.w;
+    if (LN) {
+      const float4 xv = load4(x + r * n + c);
+      const float mu = mean[r], rs = rstd[r];
+      sgm.x += d.x * (xv.x - mu) * rs;
+      sgm.y += d.y * (xv.y - mu) * rs;
+      sgm.z += d.z * (xv.z - mu) * rs;
+      sgm.w += d.w * (xv.w - mu) * rs;
+    }
   }
-  part_b[(long)blockIdx.y * n + c] = sb;
-  if (LN) part_g[(long)blockIdx.y * n + c] = sg;
+  *(float4*)(part_b + (long)blockIdx.y * n + c) = sb;
+  if (LN) *(float4*)(part_g + (long)blockIdx.y * n + c) = sgm;
 }
 
 __global__ __launch_bounds__(NT) void colsum_final_k(const float* __restrict__ part, int nchunk,
                                                      int n, float* __restrict__ out, int accumulate) {
-  const int c = blockIdx.x * NT + threadIdx.x;
+  const int c = 4 * (blockIdx.x * NT + threadIdx.x);
   if (c >= n) return;
-  float s = 0.f;
-  for (int ch = 0; ch < nchunk; ++ch) s += part[(long)ch * n + c];
-  out[c] = accumulate ? out[c] + s : s;
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int ch = 0; ch < nchunk; ++ch) {
+    const float4 v = *(const float4*)(part + (long)ch * n + c);
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  float4* o = (float4*)(out + c);
+  if (accumulate) {
+    const float4 v = *o;
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  *o = s;
 }
 
 }  // namespace
@@ -121,50 +148,35 @@ hipError_t ln_backward(int elt, const void* dout, const void* x, const float* me
   return hipGetLastError();
 }
 
-long colsum_part_floats(long rows, int n) { return 2 * ((rows + CHUNK - 1) / CHUNK) * (long)n; }
+long colsum_part_floats(long rows, int n, int nseg) {
+  return 2 * nseg * ((rows + CHUNK - 1) / CHUNK) * (long)n;
+}
 
-static hipError_t colsum_impl(int elt, bool ln, const void* dout, long ld, const void* x,
-                              const float* mean, const float* rstd, long rows, int n, float* dg,
-                              float* db, int accumulate, float* part, hipStream_t s) {
+hipError_t colsum(int elt, bool ln, const ColSegs& sg, int nseg, long ld, long rows, int n, float* dg,
+                  float* db, int accumulate, float* part, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  const int nchunk = (int)((rows + CHUNK - 1) / CHUNK);
+  if (n % 4) return hipErrorInvalidValue;
+  const int cps = (int)((rows + CHUNK - 1) / CHUNK);
+  const int nchunk = nseg * cps;
   float* part_b = part;
   float* part_g = part + (long)nchunk * n;
-  dim3 grid((n + NT - 1) / NT, nchunk);
+  const int cb = (n / 4 + NT - 1) / NT;
   if (nchunk > 0) {
+    dim3 grid(cb, nchunk);
     if (elt == 2) {
       if (ln)
-        hipLaunchKernelGGL((colsum_part_k<bf16, true>), grid, dim3(NT), 0, s, (const bf16*)dout, ld,
-                           (const bf16*)x, mean, rstd, rows, n, part_b, part_g);
+        hipLaunchKernelGGL((colsum_part_k<bf16, true>), grid, dim3(NT), 0, s, sg, ld, rows, n, cps, part_b, part_g);
       else
-        hipLaunchKernelGGL((colsum_part_k<bf16, false>), grid, dim3(NT), 0, s, (const bf16*)dout, ld,
-                           (const bf16*)nullptr, mean, rstd, rows, n, part_b, part_g);
+        hipLaunchKernelGGL((colsum_part_k<bf16, false>), grid, dim3(NT), 0, s, sg, ld, rows, n, cps, part_b, part_g);
     } else {
       if (ln)
-        hipLaunchKernelGGL((colsum_part_k<float, true>), grid, dim3(NT), 0, s, (const float*)dout, ld,
-                           (const float*)x, mean, rstd, rows, n, part_b, part_g);
+        hipLaunchKernelGGL((colsum_part_k<float, true>), grid, dim3(NT), 0, s, sg, ld, rows, n, cps, part_b, part_g);
       else
-        hipLaunchKernelGGL((colsum_part_k<float, false>), grid, dim3(NT), 0, s, (const float*)dout,
-                           ld, (const float*)nullptr, mean, rstd, rows, n, part_b, part_g);
+        hipLaunchKernelGGL((colsum_part_k<float, false>), grid, dim3(NT), 0, s, sg, ld, rows, n, cps, part_b, part_g);
     }
   }
-  dim3 g1((n + NT - 1) / NT);
-  hipLaunchKernelGGL(colsum_final_k, g1, dim3(NT), 0, s, (const float*)part_b, nchunk, n, db,
-                     accumulate);
+  hipLaunchKernelGGL(colsum_final_k, dim3(cb), dim3(NT), 0, s, (const float*)part_b, nchunk, n, db, accumulate);
   if (ln)
-    hipLaunchKernelGGL(colsum_final_k, g1, dim3(NT), 0, s, (const float*)part_g, nchunk, n, dg,
-                       accumulate);
+    hipLaunchKernelGGL(colsum_final_k, dim3(cb), dim3(NT), 0, s, (const float*)part_g, nchunk, n, dg, accumulate);
   return hipGetLastError();
-}
-
-hipError_t colsum_bias(int elt, const void* dout, long ld, long rows, int n, float* db,
-                       int accumulate, float* part, hipStream_t s) {
-  return colsum_impl(elt, false, dout, ld, nullptr, nullptr, nullptr, rows, n, nullptr, db,
-                     accumulate, part, s);
-}
-
-hipError_t colsum_ln(int elt, const void* dout, const void* x, const float* mean,
-                     const float* rstd, long rows, int n, float* dg, float* db, int accumulate,
-                     float* part, hipStream_t s) {
-  return colsum_impl(elt, true, dout, n, x, mean, rstd, rows, n, dg, db, accumulate, part, s);
 }

@@ -169,7 +169,8 @@ rc_status make_layout(const rc_stage_config* c, Layout& y) {
   y.off_S = take(ss * 4);
   y.off_dS = take(ss * E);
   y.off_dO = take(T * h * E);
-  y.off_part = take(4 * colsum_part_floats(y.T, (int)std::max(3 * h, f)));
+  y.off_part = take(4 * colsum_part_floats(y.T, (int)std::max(3 * h, f),
+                                           std::min(y.wslots, (int)GEMM_MAX_SEG)));
   y.work_bytes = o;
   return RC_OK;
 }
@@ -475,39 +476,82 @@ rc_status run_backward_input(rc_stage* st, int ws, int fs, const void* dy, void*
   return RC_OK;
 }
 
-rc_status run_backward_weight(rc_stage* st, int ws) {
+// B_weight of n micro-batches (stash slots ws[0..n)) in one pass: every
+// parameter's gradient contribution of all n is one product / reduction over
+// their concatenated tokens (segments of T tokens, one per stash slot).
+rc_status run_backward_weight(rc_stage* st, const int* ws, int n) {
   const Layout& y = st->lay;
   const int E = y.elt;
   const long T = y.T, h = y.h, f = y.f;
   const int acc = st->grads_fresh ? 0 : 1;
   hipStream_t s = st->stream;
   float* part = (float*)(st->work + y.off_part);
+  // bf16 k-tiles of 64 must not straddle two micro-batches
+  const bool fused = !y.bf || (T % 64 == 0);
   for (int l = 0; l < y.L; ++l) {
-    WPtr w = wptr(st, ws, l);
+    WPtr w[GEMM_MAX_SEG];
+    for (int q = 0; q < n; ++q) w[q] = wptr(st, ws[q], l);
     struct {
       int pid;
       long M, N;
-      char *X, *dY;
-    } lin[4] = {{RC_P_W_QKV, h, 3 * h, w.A, w.dQKV},
-                {RC_P_W_O, h, h, w.O, w.dH},
-                {RC_P_W_1, h, f, w.C, w.dU},
-                {RC_P_W_2, f, h, w.G, w.dY}};
+      char* WPtr::*X;
+      char* WPtr::*dY;
+    } lin[4] = {{RC_P_W_QKV, h, 3 * h, &WPtr::A, &WPtr::dQKV},
+                {RC_P_W_O, h, h, &WPtr::O, &WPtr::dH},
+                {RC_P_W_1, h, f, &WPtr::C, &WPtr::dU},
+                {RC_P_W_2, f, h, &WPtr::G, &WPtr::dY}};
     for (auto& q : lin) {
-      // dW (+)= X^T dY : reduction over the T tokens
-      GemmParams g = gp(q.M, q.N, T, q.X, q.M, 0, q.dY, q.N, 0, EPI_F32_ACC, gradp(st, l, q.pid), q.N);
-      g.accumulate = acc;
-      HIPCHK(gemm_lin(st, g, RC_K_GEMM_WGRAD));
+      // dW (+)= sum over the n micro-batches of X^T dY (reduction over tokens)
+      if (fused) {
+        GemmParams g = gp(q.M, q.N, T * n, nullptr, q.M, 0, nullptr, q.N, 0, EPI_F32_ACC,
+                          gradp(st, l, q.pid), q.N);
+        g.accumulate = acc;
+        g.kseg_len = (int)T;
+        for (int k = 0; k < n; ++k) {
+          g.segA[k] = w[k].*(q.X);
+          g.segB[k] = w[k].*(q.dY);
+        }
+        HIPCHK(gemm_lin(st, g, RC_K_GEMM_WGRAD));
+      } else {
+        for (int k = 0; k < n; ++k) {
+          GemmParams g = gp(q.M, q.N, T, w[k].*(q.X), q.M, 0, w[k].*(q.dY), q.N, 0, EPI_F32_ACC,
+                            gradp(st, l, q.pid), q.N);
+          g.accumulate = acc || k > 0;
+          HIPCHK(gemm_lin(st, g, RC_K_GEMM_WGRAD));
+        }
+      }
     }
     const double rb = acc ? 8.0 : 4.0;
-    Prof pr(st, RC_K_REDUCE, 0, (double)T * (6 * h + f) * E + rb * (6 * h + f) + 2.0 * T * h * E + 16.0 * T + 4 * rb * h);
-    HIPCHK(colsum_bias(E, w.dQKV, 3 * h, T, 3 * h, gradp(st, l, RC_P_B_QKV), acc, part, s));
-    HIPCHK(colsum_bias(E, w.dH, h, T, h, gradp(st, l, RC_P_B_O), acc, part, s));
-    HIPCHK(colsum_bias(E, w.dU, f, T, f, gradp(st, l, RC_P_B_1), acc, part, s));
-    HIPCHK(colsum_bias(E, w.dY, h, T, h, gradp(st, l, RC_P_B_2), acc, part, s));
-    HIPCHK(colsum_ln(E, w.dA, w.X, w.mu1, w.r1, T, h, gradp(st, l, RC_P_LN1_G),
-                     gradp(st, l, RC_P_LN1_B), acc, part, s));
-    HIPCHK(colsum_ln(E, w.dC, w.H, w.mu2, w.r2, T, h, gradp(st, l, RC_P_LN2_G),
-                     gradp(st, l, RC_P_LN2_B), acc, part, s));
+    Prof pr(st, RC_K_REDUCE, 0,
+            n * ((double)T * (6 * h + f) * E + 2.0 * T * h * E + 16.0 * T) + rb * (6 * h + f) + 4 * rb * h);
+    ColSegs sg;
+    std::memset(&sg, 0, sizeof(sg));
+    struct {
+      int pid;
+      long N;
+      char* WPtr::*D;
+    } bias[4] = {{RC_P_B_QKV, 3 * h, &WPtr::dQKV}, {RC_P_B_O, h, &WPtr::dH},
+                 {RC_P_B_1, f, &WPtr::dU}, {RC_P_B_2, h, &WPtr::dY}};
+    for (auto& b : bias) {
+      for (int k = 0; k < n; ++k) sg.dout[k] = w[k].*(b.D);
+      HIPCHK(colsum(E, false, sg, n, b.N, T, (int)b.N, nullptr, gradp(st, l, b.pid), acc, part, s));
+    }
+    for (int k = 0; k < n; ++k) {
+      sg.dout[k] = w[k].dA;
+      sg.x[k] = w[k].X;
+      sg.mean[k] = w[k].mu1;
+      sg.rstd[k] = w[k].r1;
+    }
+    HIPCHK(colsum(E, true, sg, n, h, T, (int)h, gradp(st, l, RC_P_LN1_G), gradp(st, l, RC_P_LN1_B), acc,
+                  part, s));
+    for (int k = 0; k < n; ++k) {
+      sg.dout[k] = w[k].dC;
+      sg.x[k] = w[k].H;
+      sg.mean[k] = w[k].mu2;
+      sg.rstd[k] = w[k].r2;
+    }
+    HIPCHK(colsum(E, true, sg, n, h, T, (int)h, gradp(st, l, RC_P_LN2_G), gradp(st, l, RC_P_LN2_B), acc,
+                  part, s));
   }
   return RC_OK;
 }
@@ -705,23 +749,40 @@ rc_status rc_stage_backward_input(rc_stage* st, rc_mb mb, const void* dy, void* 
   return RC_OK;
 }
 
-rc_status rc_stage_backward_weight(rc_stage* st, rc_mb mb) {
+rc_status rc_stage_backward_weight_many(rc_stage* st, const rc_mb* mbs, int32_t n) {
   if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
-  auto it = st->mbs.find(std::make_pair(mb.j, mb.k));
-  if (it == st->mbs.end() || it->second.state != 2)
-    return fail(RC_ERR_BAD_STATE, "backward_weight of micro-batch (" + std::to_string(mb.j) + "," +
-                                      std::to_string(mb.k) + ") needs a completed B and no prior W");
+  if (n < 1 || n > GEMM_MAX_SEG || !mbs)
+    return fail(RC_ERR_INVALID_ARG, "need 1 <= n <= " + std::to_string(GEMM_MAX_SEG) + " micro-batches");
+  int ws[GEMM_MAX_SEG];
+  std::vector<std::pair<int, int>> keys;
+  for (int q = 0; q < n; ++q) {
+    auto key = std::make_pair(mbs[q].j, mbs[q].k);
+    auto it = st->mbs.find(key);
+    if (it == st->mbs.end() || it->second.state != 2)
+      return fail(RC_ERR_BAD_STATE, "backward_weight of micro-batch (" + std::to_string(mbs[q].j) + "," +
+                                        std::to_string(mbs[q].k) + ") needs a completed B and no prior W");
+    if (std::find(keys.begin(), keys.end(), key) != keys.end())
+      return fail(RC_ERR_BAD_STATE, "micro-batch (" + std::to_string(mbs[q].j) + "," +
+                                        std::to_string(mbs[q].k) + ") listed twice");
+    keys.push_back(key);
+    ws[q] = it->second.ws;
+  }
   if (!st->dry) {
-    rc_status r = run_backward_weight(st, it->second.ws);
+    rc_status r = run_backward_weight(st, ws, n);
     if (r != RC_OK) return r;
   }
-  st->free_w.push_back(it->second.ws);
-  it->second.ws = -1;
-  it->second.state = 3;
+  for (int q = 0; q < n; ++q) {
+    MbRec& m = st->mbs[keys[q]];
+    st->free_w.push_back(m.ws);
+    m.ws = -1;
+    m.state = 3;
+    record(st, RC_OP_W, mbs[q].j, mbs[q].k);
+  }
   st->grads_fresh = false;
-  record(st, RC_OP_W, mb.j, mb.k);
   return RC_OK;
 }
+
+rc_status rc_stage_backward_weight(rc_stage* st, rc_mb mb) { return rc_stage_backward_weight_many(st, &mb, 1); }
 
 rc_status rc_stage_optimizer_step(rc_stage* st, float grad_scale) {
   if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");

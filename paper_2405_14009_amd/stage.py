@@ -145,6 +145,14 @@ class Stage:
         """B_weight of micro-batch (j, k): accumulate its parameter gradients."""
         L.check(self._lib.rc_stage_backward_weight(self._h, _mb(mb)))
 
+    def backward_weight_many(self, mbs) -> None:
+        """B_weight of several micro-batches in one pass (same result as one
+        call per micro-batch in this order; one product per parameter over
+        their concatenated tokens)."""
+        mbs = list(mbs)
+        arr = (L.RcMb * max(1, len(mbs)))(*[_mb(m) for m in mbs])
+        L.check(self._lib.rc_stage_backward_weight_many(self._h, arr, len(mbs)))
+
     def optimizer_step(self, grad_scale: float = 1.0) -> None:
         """This stage's AdamW step (no cross-stage synchronisation)."""
         L.check(self._lib.rc_stage_optimizer_step(self._h, float(grad_scale)))

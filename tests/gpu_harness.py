@@ -66,6 +66,8 @@ def run_gpu(cfg, ops=None, params=None, x_fn=None, dy_fn=None, stage=None, read_
                 out.dx[tuple(op.mb)] = to_host(dx)
         elif op.kind == "W":
             stage.backward_weight(op.mb)
+        elif op.kind == "W*":          # batched weight pass over a list of micro-batches
+            stage.backward_weight_many(op.mb)
         else:
             if read_state:
                 out.grads = stage.read_all(RC_READ_GRAD)

@@ -151,6 +151,65 @@ def test_dry_run_error_table_matches_oracle():
     assert st.op_log() == [tuple(r) for r in o.log]
 
 
+def group_w(ops):
+    """Consecutive W ops of an op list merged into one batched weight pass."""
+    out = []
+    for op in ops:
+        if op.kind == "W" and out and out[-1][0] == "W*" and len(out[-1][1]) < 32:
+            out[-1][1].append(op.mb)
+        elif op.kind == "W":
+            out.append(("W*", [op.mb]))
+        else:
+            out.append((op.kind, op.mb))
+    return out
+
+
+@pytest.mark.parametrize("name", list(CONFIGS) + list(TEST_CONFIGS))
+def test_dry_run_batched_weight_pass_logs_like_single_calls(name):
+    lib_or_skip()
+    from paper_2405_14009_amd import Stage
+    cfg = get_config(name)
+    ops = op_list(cfg) * 2
+    st = Stage.from_config(cfg, dry_run=True, stage_index=3, pipeline_id=0)
+    for kind, arg in group_w(ops):
+        if kind == "W*":
+            st.backward_weight_many(arg)
+        elif kind == "F":
+            st.forward(arg)
+        elif kind == "B":
+            st.backward_input(arg)
+        else:
+            st.optimizer_step()
+    ref = oracle_bookkeeping(cfg, ops)
+    assert st.op_log() == [(r[0], r[1], r[2], r[3], r[4], r[5]) for r in ref]
+
+
+def test_dry_run_batched_weight_pass_errors_are_all_or_nothing():
+    lib_or_skip()
+    import paper_2405_14009_amd as P
+    cfg = get_config("tiny").with_(n_mb=4, max_stashed_mb=4, max_inflight_mb=4)
+    st = P.Stage.from_config(cfg, dry_run=True)
+    for j in range(3):
+        st.forward(MB(j))
+    st.backward_input(MB(0))
+    st.backward_input(MB(1))
+    log0 = st.op_log()
+    # MB 2 has not run B: nothing happens to MB 0 and 1 either
+    with pytest.raises(P.BadStateError):
+        st.backward_weight_many([MB(0), MB(1), MB(2)])
+    with pytest.raises(P.BadStateError):
+        st.backward_weight_many([MB(0), MB(0)])
+    with pytest.raises(P.InvalidArgError):
+        st.backward_weight_many([])
+    assert st.op_log() == log0
+    assert st.stash_usage() == (3, 1)
+    st.backward_weight_many([MB(1), MB(0)])
+    assert [(r[1], r[2]) for r in st.op_log()[len(log0):]] == [(2, 1), (2, 0)]
+    assert st.stash_usage() == (1, 1)
+    with pytest.raises(P.BadStateError):
+        st.backward_weight_many([MB(0)])
+
+
 def test_product_fails_loudly_without_gpu():
     lib_or_skip()
     import torch

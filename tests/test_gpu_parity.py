@@ -113,6 +113,47 @@ def test_w_order_and_determinism():
             assert rel_l2(c.grads[l][p], a.grads[l][p]) < 1e-6, (l, p)
 
 
+def _grouped(ops):
+    from synth.schedules import Op
+    out = []
+    for op in ops:
+        if op.kind == "W" and out and out[-1].kind == "W*":
+            out[-1].mb.append(op.mb)
+        elif op.kind == "W":
+            out.append(Op("W*", [op.mb]))
+        else:
+            out.append(op)
+    return out
+
+
+@pytest.mark.parametrize("name,seq", [("small_bf16", None), ("small_bf16", 328), ("small_f32", None)])
+def test_batched_weight_pass(name, seq):
+    """One weight pass over several deferred micro-batches (one product per
+    parameter over their concatenated tokens; for bf16 token counts that are
+    not a multiple of 64, one product per micro-batch) equals one call per
+    micro-batch (fp32 sums in another order: rel <= 1e-6), logs the same
+    records, and matches the oracle."""
+    cfg = get_config(name)
+    if seq:
+        cfg = cfg.with_(seq=seq)
+    log(f"[batched W] {name} s={cfg.seq} b={cfg.micro_batch} T={cfg.seq * cfg.micro_batch} {cfg.dtype}")
+    ops = op_list(cfg, with_step=False)
+    fwd = [o for o in ops if o.kind != "W"]
+    ws = [o for o in ops if o.kind == "W"]
+    from synth.schedules import Op
+    a = run_gpu(cfg, fwd + ws, keep_outputs=False)
+    b = run_gpu(cfg, fwd + [Op("W*", [o.mb for o in ws])], keep_outputs=False)
+    c = run_gpu(cfg, _grouped(ops) + [Op("STEP")], keep_outputs=False)
+    assert a.log == b.log
+    for l in range(cfg.layers):
+        for p in range(12):
+            assert rel_l2(b.grads[l][p], a.grads[l][p]) < 1e-6, (l, p)
+    o = oracle.run_oplist(cfg)
+    assert c.log == [tuple(r) for r in o.stage.log]
+    zero_init = {(l, p) for l in range(cfg.layers) for p in (1, 3, 5, 7, 9, 11)}
+    compare_state(cfg, c, o, tol(cfg), zero_init if cfg.dtype == "bf16" else ())
+
+
 def test_peer_reroute_invariance_on_gpu():
     """Two peers of one stage on one GPU; the failed pipeline's micro-batches
     are re-routed round-robin; the peers' gradient sum equals the fault-free
