@@ -1,0 +1,603 @@
+// Fused attention core for bf16 stages with head dimension 128, on CDNA4
+// matrix cores (v_mfma_f32_32x32x16_bf16, fp32 accumulate).  Computes the
+// attention of the GPT block (Sec. 5 model family): per (sequence, head)
+// S = Q K^T / sqrt(d), causal mask, P = softmax(S), O = P V, and its input
+// gradient, without materialising S or P in memory:
+//
+//   forward   one pass over key blocks with a running row maximum and row sum
+//             (the softmax is rescaled as the maximum grows); O and the row
+//             log-sum-exp (base 2, of the scaled scores) are written.
+//   backward  P is recomputed from Q, K and the stored log-sum-exp;
+//             Dv = rowsum(dO o O) (= rowsum(dP o P));  dS = P o (dP - Dv);
+//             dV = P^T dO, dK = scale dS^T Q   (kernel over key blocks), and
+//             dQ = scale dS K                  (kernel over query blocks).
+//             Two kernels instead of atomics keep every sum in a fixed order,
+//             so the result is bitwise reproducible.
+//
+// Operand layout.  Q, K, V are the column blocks [Q | K | V] of the [T, 3h]
+// projection output (head j at columns j*128 of each block); O and dO are
+// [T, h] with head j at columns j*128; dQ, dK, dV are written into the same
+// three column blocks of the [T, 3h] gradient.
+//
+// MFMA layout (32x32x16): A fragment: lane l holds row l % 32, k = 8 (l / 32)
+// + 0..7; B fragment: column l % 32, same k; result: lane l holds column
+// l % 32, rows 8 (r / 4) + 4 (l / 32) + r % 4 (r = 0..15).  The kernels
+// arrange every product so that the score block comes out with one query (or
+// one key) per lane column: softmax statistics are then per lane, and the
+// score registers are directly the B fragment of the next product when the
+// k positions of that product are mapped to
+//   k = 8 (l / 32) + e  ->  token 4 (l / 32) + (e % 4) + 8 (e / 4)
+// within each 16-token step; the A fragments of that product are read with
+// ds_read_b64_tr_b16 at matching token rows.
+//
+// Tiles of [rows][128] bf16 (256 bytes per row) are staged in LDS by
+// buffer-load-to-LDS copies, 16-byte chunk c of row r stored at chunk
+// c ^ swz(r), swz(r) = 4 (r % 4) + (r / 4) % 4: both the row reads
+// (ds_read_b128, 16 consecutive rows of one chunk) and the transposing reads
+// (ds_read_b64_tr_b16, 4 consecutive rows of 4 chunks) are free of bank
+// conflicts.
+#include <cmath>
+
+#include "common.h"
+#include "kernels.h"
+#include "mfma_common.h"
+
+namespace {
+
+constexpr int HD = 128;          // head dimension
+constexpr int ROWB = 2 * HD;     // bytes per tile row
+constexpr int TILE64 = 64 * ROWB;  // bytes of a 64-row tile
+constexpr float kLog2e = 1.4426950408889634f;
+
+struct AttnArgs {
+  const bf16* qkv;  // [b*s, 3h]
+  const bf16* o;    // [b*s, h]
+  const bf16* dout; // [b*s, h]
+  bf16* out;        // forward: O [b*s, h];  backward: dQKV [b*s, 3h]
+  float* lse;       // [b, heads, s]  base-2 log-sum-exp of the scaled scores
+  float* dv;        // [b, heads, s]  rowsum(dO o O)
+  int s, heads, bh, h;
+  float scale, sl2;  // 1/sqrt(d), 1/sqrt(d) * log2(e)
+};
+
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+
+// This wave's share of the copy of a [ROWS][128] tile: rows row0.. of a
+// row-major matrix (leading dimension ld elements, rows >= nrows read as
+// zeros).  Slice g (1 KB = 4 rows) is copied by wave g % 4.
+template <int ROWS>
+__device__ __forceinline__ void load_tile(const i32x4& rs, char* tile, int wave, int lane, long ld,
+                                          int row0, int nrows) {
+  const int c = (lane & 15) ^ ((((lane >> 4) & 3) << 2) | wave);
+#pragma unroll
+  for (int j = 0; j < ROWS / 16; ++j) {
+    const int gr = row0 + 4 * wave + 16 * j + (lane >> 4);
+    const uint32_t off = gr < nrows ? (uint32_t)gr * (uint32_t)(2 * ld) + 16u * c : kOOB;
+    dma16(rs, __builtin_amdgcn_readfirstlane(lds_addr(tile) + (wave + 4 * j) * 1024), off);
+  }
+}
+
+// 64 floats (one per row of a 64-row block, rows >= nrows as zeros) into a
+// 1 KB LDS area; issued by one wave.
+__device__ __forceinline__ void load_vec64(const i32x4& rs, char* dst, int lane, int row0, int nrows) {
+  const int r = row0 + 4 * lane;
+  const uint32_t off = (lane < 16 && r < nrows) ? 4u * r : kOOB;
+  dma16(rs, __builtin_amdgcn_readfirstlane(lds_addr(dst)), off);
+}
+
+// Row read: 32-row block starting at row 0 of the tile, k-step ks (16 of the
+// 128 columns): lane l gets row l % 32, columns 16 ks + 8 (l / 32) + 0..7.
+struct RowOffs {
+  uint32_t off[HD / 16];
+  __device__ __forceinline__ void init(int lane) {
+    const int r = lane & 31;
+#pragma unroll
+    for (int ks = 0; ks < HD / 16; ++ks) off[ks] = r * ROWB + (((2 * ks + (lane >> 5)) ^ swz(r)) << 4);
+  }
+};
+__device__ __forceinline__ bf16x8 rd_row(const char* tile, const RowOffs& o, int blk, int ks) {
+  return *(const bf16x8*)(tile + o.off[ks] + blk * 32 * ROWB);
+}
+
+// Transposing read: columns 32 dblk + (l % 32) of the tile as rows (m), tile
+// rows as k: lane l gets tile rows 16 t + 4 (l / 32) + {0..3, 8..11}.
+struct TrOffs {
+  uint32_t off[HD / 32][2];
+  __device__ __forceinline__ void init(int lane) {
+    const int i = lane & 15, g = (lane >> 4) & 1, hh = lane >> 5;
+#pragma unroll
+    for (int b = 0; b < HD / 32; ++b)
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int r = 4 * hh + (i >> 2) + 8 * half;
+        const int c = 4 * b + 2 * g + ((i & 3) >> 1);
+        off[b][half] = r * ROWB + ((c ^ swz(r)) << 4) + 8 * (i & 1);
+      }
+  }
+};
+__device__ __forceinline__ bf16x8 rd_tr(const char* tile, const TrOffs& o, int dblk, int t) {
+  const char* p0 = tile + o.off[dblk][0] + t * 16 * ROWB;
+  const char* p1 = tile + o.off[dblk][1] + t * 16 * ROWB;
+  s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p0);
+  s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p1);
+  s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+__device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// B fragment of 16-token step t from a pair of score blocks (32 tokens each):
+// elements r = 8 (t % 2) .. +7 of block t / 2, rounded to bf16.
+__device__ __forceinline__ bf16x8 pack_frag(const f32x16 (&p)[2], int t) {
+  bf16x8 v;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = (bf16)p[t >> 1][8 * (t & 1) + e];
+  return v;
+}
+
+// Global 16-byte fragment of a stationary operand: row `row` (zeros when
+// row >= nrows), columns 16 ks + 8 (l / 32) + 0..7.
+__device__ __forceinline__ void load_stationary(bf16x8 (&f)[HD / 16], const bf16* base, long ld, int row,
+                                                int nrows, int lane) {
+#pragma unroll
+  for (int ks = 0; ks < HD / 16; ++ks) {
+    if (row < nrows) {
+      f[ks] = *(const bf16x8*)(base + (long)row * ld + 16 * ks + 8 * (lane >> 5));
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[ks][e] = (bf16)0.f;
+    }
+  }
+}
+
+// Store a [128 (d) x 32 (tokens)] accumulator set (result layout: lane column
+// = token, rows = d) as rows of a row-major bf16 matrix: 8-byte pieces.
+__device__ __forceinline__ void store_dT(const f32x16 (&acc)[HD / 32], bf16* base, long ld, int row,
+                                         int nrows, int lane, float mul) {
+  if (row >= nrows) return;
+  bf16* p = base + (long)row * ld + 4 * (lane >> 5);
+#pragma unroll
+  for (int b = 0; b < HD / 32; ++b)
+#pragma unroll
+    for (int rg = 0; rg < 4; ++rg) {
+      bf16 t[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) t[e] = (bf16)(acc[b][4 * rg + e] * mul);
+      *(uint2*)(p + 32 * b + 8 * rg) = *(const uint2*)t;
+    }
+}
+
+__device__ __forceinline__ void zero(f32x16& a) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) a[r] = 0.f;
+}
+
+// Workgroup -> (sequence*head z, block index) with the longest blocks first.
+__device__ __forceinline__ void block_of(const AttnArgs& p, int nblk, bool longest_last_index, int& z,
+                                         int& blk) {
+  const int x = blockIdx.x;
+  z = x % p.bh;
+  const int q = x / p.bh;
+  blk = longest_last_index ? nblk - 1 - q : q;
+}
+
+// ---------------------------------------------------------------------------
+// Forward.  Workgroup: 128 queries of one (sequence, head), 4 waves x 32
+// queries; key blocks of 64 staged in LDS (K and V, two stages).  Per wave and
+// key block: S^T = K Q^T (16 MFMAs, Q stationary in registers), online
+// softmax per lane (= per query), O^T += V^T P^T (16 MFMAs).
+template <bool CAUSAL>
+__global__ __launch_bounds__(256) void attn_fwd_k(AttnArgs p) {
+  __shared__ __attribute__((aligned(1024))) char lds0[2 * TILE64];
+  __shared__ __attribute__((aligned(1024))) char lds1[2 * TILE64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nqb = (p.s + 127) / 128;
+  int z, qb;
+  block_of(p, nqb, CAUSAL, z, qb);
+  const int zb = z / p.heads, zh = z % p.heads;
+  const long ld = 3L * p.h;
+  const bf16* Q = p.qkv + (long)zb * p.s * ld + zh * HD;
+  const bf16* K = Q + p.h;
+  const bf16* V = Q + 2 * p.h;
+  const i32x4 rk = make_rsrc(K, 2L * p.s * ld);
+  const i32x4 rv = make_rsrc(V, 2L * p.s * ld);
+  const int q0 = qb * 128 + 32 * wave;
+  const int qq = q0 + (lane & 31);
+
+  bf16x8 qf[HD / 16];
+  load_stationary(qf, Q, ld, qq, p.s, lane);
+  RowOffs ro;
+  ro.init(lane);
+  TrOffs to;
+  to.init(lane);
+
+  f32x16 o[HD / 32];
+#pragma unroll
+  for (int b = 0; b < HD / 32; ++b) zero(o[b]);
+  float m_run = -1e30f, l_run = 0.f;
+
+  const int nkb_all = (p.s + 63) / 64;
+  const int nkb = CAUSAL ? min(nkb_all, 2 * qb + 2) : nkb_all;
+
+  auto issue = [&](char* st, int kb) {
+    load_tile<64>(rk, st, wave, lane, ld, kb * 64, p.s);
+    load_tile<64>(rv, st + TILE64, wave, lane, ld, kb * 64, p.s);
+  };
+  auto compute = [&](const char* st, int kb) {
+    const int k0 = kb * 64;
+    if (CAUSAL && k0 > q0 + 31) return;  // every key of the block is after every query of the wave
+    const char* kt = st;
+    const char* vt = st + TILE64;
+    f32x16 sc[2];
+    zero(sc[0]);
+    zero(sc[1]);
+#pragma unroll
+    for (int ks = 0; ks < HD / 16; ++ks)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) sc[j] = mfma(rd_row(kt, ro, j, ks), qf[ks], sc[j]);
+    const bool need_mask = (CAUSAL && k0 + 63 > q0) || (k0 + 64 > p.s);
+    float mx = -1e30f;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float x = sc[j][r] * p.sl2;
+        if (need_mask) {
+          const int key = k0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (key >= p.s || (CAUSAL && key > qq)) x = -INFINITY;
+        }
+        sc[j][r] = x;
+        mx = fmaxf(mx, x);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    float ls = 0.f;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float e = __builtin_amdgcn_exp2f(sc[j][r] - m_new);
+        sc[j][r] = e;
+        ls += e;
+      }
+    l_run = l_run * alpha + ls;
+#pragma unroll
+    for (int b = 0; b < HD / 32; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[b][r] *= alpha;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const bf16x8 pf = pack_frag(sc, t);
+#pragma unroll
+      for (int b = 0; b < HD / 32; ++b) o[b] = mfma(rd_tr(vt, to, b, t), pf, o[b]);
+    }
+  };
+
+  if (nkb > 0) issue(lds0, 0);
+  stage_sync();
+  int kb = 0;
+  for (; kb + 1 < nkb; kb += 2) {
+    issue(lds1, kb + 1);
+    compute(lds0, kb);
+    stage_sync();
+    if (kb + 2 < nkb) issue(lds0, kb + 2);
+    compute(lds1, kb + 1);
+    stage_sync();
+  }
+  if (kb < nkb) compute(lds0, kb);
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float inv = 1.0f / l_tot;
+  store_dT(o, (bf16*)p.out + (long)zb * p.s * p.h + zh * HD, p.h, qq, p.s, lane, inv);
+  if (lane < 32 && qq < p.s) p.lse[(long)z * p.s + qq] = m_run + __builtin_amdgcn_logf(l_tot);
+}
+
+// Dv[z, q] = sum_d dO[q, d] O[q, d] for every (sequence, head, query):
+// 16 threads per row, 8 columns each.
+__global__ __launch_bounds__(256) void attn_dot_k(AttnArgs p, long rows) {
+  const long R = (long)blockIdx.x * 16 + (threadIdx.x >> 4);
+  if (R >= rows) return;
+  const int c = 8 * (threadIdx.x & 15);
+  const long tok = R / p.heads;
+  const int zh = (int)(R % p.heads);
+  const long off = tok * p.h + zh * HD + c;
+  const uint4 a = *(const uint4*)(p.dout + off);
+  const uint4 b = *(const uint4*)(p.o + off);
+  const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+  float acc = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    acc += __uint_as_float(av[i] << 16) * __uint_as_float(bv[i] << 16);
+    acc += __uint_as_float(av[i] & 0xffff0000u) * __uint_as_float(bv[i] & 0xffff0000u);
+  }
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 16);
+  if ((threadIdx.x & 15) == 0) {
+    const long zb = tok / p.s, q = tok % p.s;
+    p.dv[(zb * p.heads + zh) * p.s + q] = acc;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Backward over key blocks: dK, dV.  Workgroup: 128 keys of one (sequence,
+// head), 4 waves x 32 keys (K and V rows stationary in registers); query
+// blocks of 64 staged in LDS (Q, dO, log-sum-exp and Dv; two stages).  Per
+// wave and query block: S = Q K^T and dP = dO V^T (lane column = key),
+// P = exp2(S sl2 - lse), dS = P (dP - Dv); dV^T += dO^T P, dK^T += Q^T dS.
+template <bool CAUSAL>
+__global__ __launch_bounds__(256) void attn_bwd_kv_k(AttnArgs p) {
+  constexpr int STAGE = 2 * TILE64 + 2048;
+  __shared__ __attribute__((aligned(1024))) char lds0[STAGE];
+  __shared__ __attribute__((aligned(1024))) char lds1[STAGE];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nkb = (p.s + 127) / 128;
+  int z, kb;
+  block_of(p, nkb, false, z, kb);
+  const int zb = z / p.heads, zh = z % p.heads;
+  const long ld = 3L * p.h;
+  const bf16* Q = p.qkv + (long)zb * p.s * ld + zh * HD;
+  const bf16* K = Q + p.h;
+  const bf16* V = Q + 2 * p.h;
+  const bf16* dO = p.dout + (long)zb * p.s * p.h + zh * HD;
+  const i32x4 rq = make_rsrc(Q, 2L * p.s * ld);
+  const i32x4 rdo = make_rsrc(dO, 2L * p.s * p.h);
+  const i32x4 rl = make_rsrc(p.lse + (long)z * p.s, 4L * p.s);
+  const i32x4 rd = make_rsrc(p.dv + (long)z * p.s, 4L * p.s);
+  const int k0w = kb * 128 + 32 * wave;
+  const int key = k0w + (lane & 31);
+
+  bf16x8 kf[HD / 16], vf[HD / 16];
+  load_stationary(kf, K, ld, key, p.s, lane);
+  load_stationary(vf, V, ld, key, p.s, lane);
+  RowOffs ro;
+  ro.init(lane);
+  TrOffs to;
+  to.init(lane);
+
+  f32x16 dk[HD / 32], dv[HD / 32];
+#pragma unroll
+  for (int b = 0; b < HD / 32; ++b) {
+    zero(dk[b]);
+    zero(dv[b]);
+  }
+  const int nqb_all = (p.s + 63) / 64;
+  const int qb0 = CAUSAL ? 2 * kb : 0;
+
+  auto issue = [&](char* st, int qb) {
+    load_tile<64>(rq, st, wave, lane, ld, qb * 64, p.s);
+    load_tile<64>(rdo, st + TILE64, wave, lane, p.h, qb * 64, p.s);
+    if (wave == 0) load_vec64(rl, st + 2 * TILE64, lane, qb * 64, p.s);
+    if (wave == 1) load_vec64(rd, st + 2 * TILE64 + 1024, lane, qb * 64, p.s);
+  };
+  auto compute = [&](const char* st, int qb) {
+    const int qs = qb * 64;
+    if (CAUSAL && qs + 63 < k0w) return;  // every query of the block precedes every key of the wave
+    const char* qt = st;
+    const char* ot = st + TILE64;
+    const float* lse = (const float*)(st + 2 * TILE64);
+    const float* dvv = (const float*)(st + 2 * TILE64 + 1024);
+    f32x16 sc[2], dp[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      zero(sc[j]);
+      zero(dp[j]);
+    }
+#pragma unroll
+    for (int ks = 0; ks < HD / 16; ++ks)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        sc[j] = mfma(rd_row(qt, ro, j, ks), kf[ks], sc[j]);
+        dp[j] = mfma(rd_row(ot, ro, j, ks), vf[ks], dp[j]);
+      }
+    const bool need_mask = CAUSAL && qs < k0w + 31;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        const int ql = 32 * j + 8 * rg + 4 * (lane >> 5);
+        const float4 L4 = *(const float4*)(lse + ql);
+        const float4 D4 = *(const float4*)(dvv + ql);
+        const float Lv[4] = {L4.x, L4.y, L4.z, L4.w}, Dv[4] = {D4.x, D4.y, D4.z, D4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * rg + e;
+          float pv = __builtin_amdgcn_exp2f(sc[j][r] * p.sl2 - Lv[e]);
+          if (need_mask && key > qs + ql + e) pv = 0.f;
+          sc[j][r] = pv;
+          dp[j][r] = pv * (dp[j][r] - Dv[e]);
+        }
+      }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const bf16x8 pf = pack_frag(sc, t);
+      const bf16x8 sf = pack_frag(dp, t);
+#pragma unroll
+      for (int b = 0; b < HD / 32; ++b) {
+        dv[b] = mfma(rd_tr(ot, to, b, t), pf, dv[b]);
+        dk[b] = mfma(rd_tr(qt, to, b, t), sf, dk[b]);
+      }
+    }
+  };
+
+  const int n = nqb_all - qb0;
+  if (n > 0) issue(lds0, qb0);
+  stage_sync();
+  int i = 0;
+  for (; i + 1 < n; i += 2) {
+    issue(lds1, qb0 + i + 1);
+    compute(lds0, qb0 + i);
+    stage_sync();
+    if (i + 2 < n) issue(lds0, qb0 + i + 2);
+    compute(lds1, qb0 + i + 1);
+    stage_sync();
+  }
+  if (i < n) compute(lds0, qb0 + i);
+
+  bf16* dK = p.out + (long)zb * p.s * ld + p.h + zh * HD;
+  store_dT(dk, dK, ld, key, p.s, lane, p.scale);
+  store_dT(dv, dK + p.h, ld, key, p.s, lane, 1.0f);
+}
+
+// Backward over query blocks: dQ.  Workgroup: 128 queries, 4 waves x 32
+// (Q and dO rows stationary); key blocks of 64 staged in LDS (K, V).  Per
+// wave and key block: S^T = K Q^T, dP^T = V dO^T (lane column = query),
+// P, dS as above; dQ^T += K^T dS^T.
+template <bool CAUSAL>
+__global__ __launch_bounds__(256) void attn_bwd_q_k(AttnArgs p) {
+  __shared__ __attribute__((aligned(1024))) char lds0[2 * TILE64];
+  __shared__ __attribute__((aligned(1024))) char lds1[2 * TILE64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nqb = (p.s + 127) / 128;
+  int z, qb;
+  block_of(p, nqb, CAUSAL, z, qb);
+  const int zb = z / p.heads, zh = z % p.heads;
+  const long ld = 3L * p.h;
+  const bf16* Q = p.qkv + (long)zb * p.s * ld + zh * HD;
+  const bf16* K = Q + p.h;
+  const bf16* V = Q + 2 * p.h;
+  const bf16* dO = p.dout + (long)zb * p.s * p.h + zh * HD;
+  const i32x4 rk = make_rsrc(K, 2L * p.s * ld);
+  const i32x4 rv = make_rsrc(V, 2L * p.s * ld);
+  const int q0 = qb * 128 + 32 * wave;
+  const int qq = q0 + (lane & 31);
+
+  bf16x8 qf[HD / 16], of[HD / 16];
+  load_stationary(qf, Q, ld, qq, p.s, lane);
+  load_stationary(of, dO, p.h, qq, p.s, lane);
+  const float Lq = qq < p.s ? p.lse[(long)z * p.s + qq] : 0.f;
+  const float Dq = qq < p.s ? p.dv[(long)z * p.s + qq] : 0.f;
+  RowOffs ro;
+  ro.init(lane);
+  TrOffs to;
+  to.init(lane);
+
+  f32x16 dq[HD / 32];
+#pragma unroll
+  for (int b = 0; b < HD / 32; ++b) zero(dq[b]);
+  const int nkb_all = (p.s + 63) / 64;
+  const int nkb = CAUSAL ? min(nkb_all, 2 * qb + 2) : nkb_all;
+
+  auto issue = [&](char* st, int kb) {
+    load_tile<64>(rk, st, wave, lane, ld, kb * 64, p.s);
+    load_tile<64>(rv, st + TILE64, wave, lane, ld, kb * 64, p.s);
+  };
+  auto compute = [&](const char* st, int kb) {
+    const int k0 = kb * 64;
+    if (CAUSAL && k0 > q0 + 31) return;
+    const char* kt = st;
+    const char* vt = st + TILE64;
+    f32x16 sc[2], dp[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      zero(sc[j]);
+      zero(dp[j]);
+    }
+#pragma unroll
+    for (int ks = 0; ks < HD / 16; ++ks)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        sc[j] = mfma(rd_row(kt, ro, j, ks), qf[ks], sc[j]);
+        dp[j] = mfma(rd_row(vt, ro, j, ks), of[ks], dp[j]);
+      }
+    const bool need_mask = (CAUSAL && k0 + 63 > q0) || (k0 + 64 > p.s);
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float pv = __builtin_amdgcn_exp2f(sc[j][r] * p.sl2 - Lq);
+        if (need_mask) {
+          const int key = k0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (key >= p.s || (CAUSAL && key > qq)) pv = 0.f;
+        }
+        dp[j][r] = pv * (dp[j][r] - Dq);
+      }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const bf16x8 sf = pack_frag(dp, t);
+#pragma unroll
+      for (int b = 0; b < HD / 32; ++b) dq[b] = mfma(rd_tr(kt, to, b, t), sf, dq[b]);
+    }
+  };
+
+  if (nkb > 0) issue(lds0, 0);
+  stage_sync();
+  int kb = 0;
+  for (; kb + 1 < nkb; kb += 2) {
+    issue(lds1, kb + 1);
+    compute(lds0, kb);
+    stage_sync();
+    if (kb + 2 < nkb) issue(lds0, kb + 2);
+    compute(lds1, kb + 1);
+    stage_sync();
+  }
+  if (kb < nkb) compute(lds0, kb);
+
+  store_dT(dq, p.out + (long)zb * p.s * ld + zh * HD, ld, qq, p.s, lane, p.scale);
+}
+
+AttnArgs make_args(const void* qkv, int b, int s, int heads, int h) {
+  AttnArgs a;
+  a.qkv = (const bf16*)qkv;
+  a.o = nullptr;
+  a.dout = nullptr;
+  a.out = nullptr;
+  a.lse = nullptr;
+  a.dv = nullptr;
+  a.s = s;
+  a.heads = heads;
+  a.bh = b * heads;
+  a.h = h;
+  a.scale = 1.0f / std::sqrt((float)HD);
+  a.sl2 = a.scale * kLog2e;
+  return a;
+}
+
+}  // namespace
+
+bool attn_flash_supported(int elt, int head_dim) { return elt == 2 && head_dim == HD; }
+
+hipError_t attn_flash_forward(const void* qkv, void* o, float* lse, int b, int s, int heads, int h,
+                              int causal, hipStream_t st) {
+  if (h != heads * HD) return hipErrorInvalidValue;
+  if (b <= 0 || s <= 0) return hipSuccess;
+  AttnArgs a = make_args(qkv, b, s, heads, h);
+  a.out = (bf16*)o;
+  a.lse = lse;
+  const dim3 grid(((s + 127) / 128) * a.bh);
+  if (causal)
+    hipLaunchKernelGGL(attn_fwd_k<true>, grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL(attn_fwd_k<false>, grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t attn_flash_backward(const void* qkv, const void* o, const void* dout, const float* lse,
+                               float* dv_scratch, void* dqkv, int b, int s, int heads, int h, int causal,
+                               hipStream_t st) {
+  if (h != heads * HD) return hipErrorInvalidValue;
+  if (b <= 0 || s <= 0) return hipSuccess;
+  AttnArgs a = make_args(qkv, b, s, heads, h);
+  a.o = (const bf16*)o;
+  a.dout = (const bf16*)dout;
+  a.out = (bf16*)dqkv;
+  a.lse = (float*)lse;
+  a.dv = dv_scratch;
+  const long rows = (long)b * s * heads;
+  hipLaunchKernelGGL(attn_dot_k, dim3((unsigned)((rows + 15) / 16)), dim3(256), 0, st, a, rows);
+  const dim3 grid(((s + 127) / 128) * a.bh);
+  if (causal) {
+    hipLaunchKernelGGL(attn_bwd_kv_k<true>, grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL(attn_bwd_q_k<true>, grid, dim3(256), 0, st, a);
+  } else {
+    hipLaunchKernelGGL(attn_bwd_kv_k<false>, grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL(attn_bwd_q_k<false>, grid, dim3(256), 0, st, a);
+  }
+  return hipGetLastError();
+}

@@ -41,6 +41,20 @@ hipError_t softmax_forward(int elt, const float* S, void* P, long rows, int s, f
 hipError_t softmax_backward(int elt, const float* dP, const void* P, void* dS, long rows, int s,
                             float scale, int causal, hipStream_t st);
 
+// Fused attention core (bf16, head dimension 128): per (sequence, head)
+// O = softmax(Q K^T / sqrt(128), causal) V without materialising the scores.
+// qkv: [b*s, 3h] with column blocks Q | K | V (head j at columns j*128 of each);
+// o: [b*s, h]; lse: [b, heads, s] fp32 base-2 log-sum-exp of the scaled scores
+// (written by the forward, read by the backward).  The backward writes dQ, dK,
+// dV into the three column blocks of dqkv [b*s, 3h]; dv_scratch holds b*heads*s
+// floats.  h == heads * 128.
+bool attn_flash_supported(int elt, int head_dim);
+hipError_t attn_flash_forward(const void* qkv, void* o, float* lse, int b, int s, int heads, int h,
+                              int causal, hipStream_t st);
+hipError_t attn_flash_backward(const void* qkv, const void* o, const void* dout, const float* lse,
+                               float* dv_scratch, void* dqkv, int b, int s, int heads, int h, int causal,
+                               hipStream_t st);
+
 // AdamW over n fp32 parameters; weight decay on indices < n_decay; when wb is
 // non-null the first n_decay updated values are also written to it in bf16.
 hipError_t adamw_step(float* p, const float* g, float* m, float* v, void* wb, long n, long n_decay,

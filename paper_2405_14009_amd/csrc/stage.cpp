@@ -60,13 +60,13 @@ struct WLayer {
 };
 // Byte offsets inside one layer of a forward-only slot.
 struct FLayer {
-  size_t QKV, U, P, bytes;
+  size_t QKV, U, P, bytes;  // P: attention probabilities, or the row log-sum-exp (fused attention)
 };
 
 struct Layout {
   int L, h, a, d, f, s, b, elt, causal;
   long T;
-  bool bf;
+  bool bf, flash;
   float eps;
   int wslots, fslots;
   std::vector<std::array<PLoc, RC_NUM_PARAMS>> p;
@@ -75,7 +75,7 @@ struct Layout {
   WLayer w;
   FLayer fl;
   size_t wslot_bytes, fslot_bytes, off_fslots, stash_bytes;
-  size_t off_S, off_dS, off_dO, off_part, work_bytes;
+  size_t off_S, off_dS, off_dO, off_dv, off_part, work_bytes;
 };
 
 rc_status make_layout(const rc_stage_config* c, Layout& y) {
@@ -102,6 +102,7 @@ rc_status make_layout(const rc_stage_config* c, Layout& y) {
   y.T = (long)c->micro_batch * c->seq_len;
   y.bf = c->dtype == RC_BF16;
   y.elt = y.bf ? 2 : 4;
+  y.flash = attn_flash_supported(y.elt, d);
   y.causal = c->causal;
   y.eps = c->ln_eps;
   y.wslots = c->max_stashed_mb;
@@ -157,18 +158,20 @@ rc_status make_layout(const rc_stage_config* c, Layout& y) {
   w.bytes = o;
   o = 0;
   const size_t ss = (size_t)y.b * y.a * y.s * y.s;
+  const size_t rows = (size_t)y.b * y.a * y.s;
   y.fl.QKV = take(T * 3 * h * E);
   y.fl.U = take(T * f * E);
-  y.fl.P = take(ss * E);
+  y.fl.P = take(y.flash ? rows * 4 : ss * E);
   y.fl.bytes = o;
   y.wslot_bytes = (size_t)y.L * w.bytes;
   y.fslot_bytes = (size_t)y.L * y.fl.bytes;
   y.off_fslots = (size_t)y.wslots * y.wslot_bytes;
   y.stash_bytes = y.off_fslots + (size_t)y.fslots * y.fslot_bytes;
   o = 0;
-  y.off_S = take(ss * 4);
-  y.off_dS = take(ss * E);
+  y.off_S = take(y.flash ? 0 : ss * 4);
+  y.off_dS = take(y.flash ? 0 : ss * E);
   y.off_dO = take(T * h * E);
+  y.off_dv = take(y.flash ? rows * 4 : 0);
   y.off_part = take(4 * colsum_part_floats(y.T, (int)std::max(3 * h, f),
                                            std::min(y.wslots, (int)GEMM_MAX_SEG)));
   y.work_bytes = o;
@@ -332,6 +335,10 @@ void batch_heads(GemmParams& g, const Layout& y, long a_bs, long a_hs, long b_bs
 rc_status attn_forward(rc_stage* st, char* QKV, char* P, char* O) {
   const Layout& y = st->lay;
   const int E = y.elt;
+  if (y.flash) {
+    HIPCHK(attn_flash_forward(QKV, O, (float*)P, y.b, y.s, y.a, y.h, y.causal, st->stream));
+    return RC_OK;
+  }
   const long s = y.s, h = y.h, d = y.d, ss = s * s;
   float* S = (float*)(st->work + y.off_S);
   GemmParams g = gp(y.s, y.s, y.d, QKV, 3 * h, 1, el(QKV, h, E), 3 * h, 1, EPI_F32_STORE, S, s);
@@ -347,9 +354,14 @@ rc_status attn_forward(rc_stage* st, char* QKV, char* P, char* O) {
   return RC_OK;
 }
 
-rc_status attn_backward(rc_stage* st, char* QKV, char* P, char* dO, char* dQKV) {
+rc_status attn_backward(rc_stage* st, char* QKV, char* P, char* O, char* dO, char* dQKV) {
   const Layout& y = st->lay;
   const int E = y.elt;
+  if (y.flash) {
+    HIPCHK(attn_flash_backward(QKV, O, dO, (const float*)P, (float*)(st->work + y.off_dv), dQKV, y.b,
+                               y.s, y.a, y.h, y.causal, st->stream));
+    return RC_OK;
+  }
   const long s = y.s, h = y.h, d = y.d, ss = s * s;
   float* dP = (float*)(st->work + y.off_S);
   char* dS = st->work + y.off_dS;
@@ -462,7 +474,7 @@ rc_status run_backward_input(rc_stage* st, int ws, int fs, const void* dy, void*
     HIPCHK(gemm_lin(st, g, RC_K_GEMM_DGRAD));
     {
       Prof pa(st, RC_K_ATTN_BWD, 4.0 * att, 8.0 * T * h * E);
-      rc_status r = attn_backward(st, fl.QKV, fl.P, dO, w.dQKV);
+      rc_status r = attn_backward(st, fl.QKV, fl.P, w.O, dO, w.dQKV);
       if (r != RC_OK) return r;
     }
     // dA = dQKV W_qkv^T
