@@ -1,12 +1,13 @@
 // bf16 GEMM kernel template on CDNA4 matrix cores: v_mfma_f32_32x32x16_bf16,
 // fp32 accumulate.
 //
-// Tiles.  A BM x BN workgroup tile runs 4 waves in a 2 x 2 grid (one per
-// SIMD); each wave owns a (BM/2) x (BN/2) tile of 32x32 MFMA blocks: 128 x 128
-// (256 fp32 accumulators) for 256x256 tiles, 128 x 64 for 256x128 tiles.
-// LDS bandwidth, not MFMA issue, bounds these kernels once operands are
-// staged through LDS, so the larger wave tile (8 fragment reads per 16 MFMAs
-// instead of 6 per 8) is the main lever.
+// Tiles.  A BM x BN workgroup tile runs NW waves in a 2 x NW/2 grid; each
+// wave owns a 128 x (BN / (NW/2)) tile of 32x32 MFMA blocks.  The launcher
+// uses NW = 8: 128 x 64 wave tiles for 256x256 tiles and 128 x 32 for 256x128
+// tiles, two waves per SIMD.  With one wave per SIMD (NW = 4, 128 x 128 wave
+// tiles) every barrier, LDS-read wait and full memory-instruction queue left
+// the matrix core idle; with two, the other wave issues MFMAs meanwhile, which
+// measured faster on every stage shape despite the smaller wave tiles.
 //
 // Staging.  k-tiles of 64 are copied from memory straight into LDS by
 // buffer-load-to-LDS instructions (each wave instruction deposits 64 lanes x
@@ -41,10 +42,10 @@ __device__ __forceinline__ int swz_k(int r) { return (r & 7) ^ ((r >> 3) & 3); }
 __device__ __forceinline__ int swz_mn(int r) { return (r & 3) << 2; }
 
 // One operand's share of the per-k-tile copy: this wave issues instructions
-// g = wave + 4 q (q < NI) of the operand's 1 KB slices.  Every slice of a wave
+// g = wave + NW q (q < NI) of the operand's 1 KB slices (NW waves).  Every slice of a wave
 // differs from its first by a fixed row (k-contiguous) or k-row
 // (m/n-contiguous) step, so two per-lane values describe all of them.
-template <int ROWS, bool KC, int NI>
+template <int ROWS, bool KC, int NI, int NW>
 struct Copier {
   uint32_t base;  // byte offset of this lane's row (k-contiguous) / column (m/n-contiguous) in slice 0
   int kk;         // k offset of this lane's data within the k-tile, slice 0
@@ -72,13 +73,13 @@ struct Copier {
       uint32_t off;
       if (KC) {
         const int k = k0 + kk;
-        const bool ok = (mn + 32 * q < MN) && (k < K);
-        off = ok ? base + (uint32_t)(32 * q) * (uint32_t)(2 * ld) + 2u * k : kOOB;
+        const bool ok = (mn + 8 * NW * q < MN) && (k < K);
+        off = ok ? base + (uint32_t)(8 * NW * q) * (uint32_t)(2 * ld) + 2u * k : kOOB;
       } else {
-        const int k = k0 + kk + 4 * RPI * q;
+        const int k = k0 + kk + NW * RPI * q;
         off = (mn < MN && k < K) ? base + (uint32_t)k * (uint32_t)(2 * ld) : kOOB;
       }
-      dma16(r, __builtin_amdgcn_readfirstlane(lds_addr(tile) + (wave + 4 * q) * 1024), off);
+      dma16(r, __builtin_amdgcn_readfirstlane(lds_addr(tile) + (wave + NW * q) * 1024), off);
     }
   }
 };
@@ -202,11 +203,11 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, f32x16 (&acc)[4][T
   }
 }
 
-template <int BM, int BN, bool AK, bool BKC, int EPI>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
-  static_assert(BM == 256 && (BN == 256 || BN == 128), "tile shapes");
-  constexpr int WN_ = 2, NW = 4;
-  constexpr int TN = BN / 64;  // 32-wide blocks per wave along n
+template <int BM, int BN, int NW, bool AK, bool BKC, int EPI>
+__global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
+  static_assert(BM == 256 && (BN == 256 || BN == 128) && (NW == 4 || NW == 8), "tile shapes");
+  constexpr int WN_ = NW / 2;            // waves along n (2 along m)
+  constexpr int TN = BN / (32 * WN_);    // 32-wide blocks per wave along n
   constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
   constexpr int STAGE = A_BYTES + B_BYTES;
   constexpr int NA = A_BYTES / 1024, NB = B_BYTES / 1024;  // wave instructions per k-tile
@@ -249,14 +250,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
   else if (p.krange == KR_ABOVE) kb = (m0 / BK) * BK;
   const int nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
 
-  Copier<BM, AK, NIA> ca;
-  Copier<BN, BKC, NIB> cb;
+  Copier<BM, AK, NIA, NW> ca;
+  Copier<BN, BKC, NIB, NW> cb;
   ca.init(wave, p.lda, m0, lane);
   cb.init(wave, p.ldb, n0, lane);
   FragOffsets<BM, AK, 4> fa;
   FragOffsets<BN, BKC, TN> fb;
   fa.init(wm * 128, lane);
-  fb.init(wn * (BN / 2), lane);
+  fb.init(wn * (BN / WN_), lane);
 
   f32x16 acc[4][TN];
 #pragma unroll
@@ -299,9 +300,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmParams p) {
   // LDS is free once every wave is past its last k-tile.
   __syncthreads();
   constexpr int EPI_BYTES = 32 * (32 * TN + 8) * 4;  // one wave's block-row tile
-  static_assert(2 * EPI_BYTES <= STAGE, "epilogue tiles fit two per stage");
-  float* sm = (float*)((wave < 2 ? lds0 : lds1) + (wave & 1) * EPI_BYTES);
-  epilogue<EPI, TN>(p, acc, sm, m0 + wm * 128, n0 + wn * (BN / 2), lane, c_off);
+  static_assert((NW / 2) * EPI_BYTES <= STAGE, "epilogue tiles fit NW/2 per stage");
+  float* sm = (float*)((wave < NW / 2 ? lds0 : lds1) + (wave % (NW / 2)) * EPI_BYTES);
+  epilogue<EPI, TN>(p, acc, sm, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
 }
 
 template <bool AK, bool BKC, int EPI>
@@ -314,12 +315,14 @@ hipError_t launch_bf16(const GemmParams& p, hipStream_t s) {
   // Tile choice: the fewest (waves of 256 workgroups) x (tile area), i.e. the
   // least padded work on 256 compute units; ties go to the larger tile, which
   // re-reads its operands less.
+  // 8 waves (2 per SIMD): while one wave of a SIMD waits on a barrier or
+  // its LDS reads, the other issues MFMAs.
   if (p.N <= 128 || cost(256, 128) < cost(256, 256)) {
     const int tiles = ((p.M + 255) / 256) * ((p.N + 127) / 128);
-    hipLaunchKernelGGL((gemm_bf16_kernel<256, 128, AK, BKC, EPI>), dim3(tiles, z), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((gemm_bf16_kernel<256, 128, 8, AK, BKC, EPI>), dim3(tiles, z), dim3(512), 0, s, p);
   } else {
     const int tiles = ((p.M + 255) / 256) * ((p.N + 255) / 256);
-    hipLaunchKernelGGL((gemm_bf16_kernel<256, 256, AK, BKC, EPI>), dim3(tiles, z), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((gemm_bf16_kernel<256, 256, 8, AK, BKC, EPI>), dim3(tiles, z), dim3(512), 0, s, p);
   }
   return hipGetLastError();
 }

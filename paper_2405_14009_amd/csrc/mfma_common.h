@@ -50,9 +50,14 @@ __device__ __forceinline__ uint32_t lds_addr(const char* p) {
 
 // vmcnt(0): this thread's copies have landed; the barrier then makes every
 // wave's copies visible and frees the stage just read for the next copy.
+// The scheduling fences keep the wait after every MFMA of the stage just
+// computed (the scheduler would otherwise hoist it above MFMAs, which touch
+// no memory, and shrink the time the next stage's copy has to land).
 __device__ __forceinline__ void stage_sync() {
+  __builtin_amdgcn_sched_barrier(0);
   __builtin_amdgcn_s_waitcnt(0x0F70);
   __syncthreads();
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 }  // namespace
