@@ -44,7 +44,8 @@ def workload_name(cfg) -> str:
 
 def cpu_baseline(cfg, params) -> dict:
     """The fp64 oracle (as it stands) on a bounded sample of the workload:
-    F + B_input + B_weight of one layer for one micro-batch at full shape."""
+    F + B_input + B_weight of one layer at full shape, for successive
+    micro-batches until at least 10 s of CPU work have run."""
     import numpy as np
     import oracle
     from synth import gen_dy, gen_x
@@ -54,20 +55,44 @@ def cpu_baseline(cfg, params) -> dict:
     except Exception:
         cores = len(os.sched_getaffinity(0))
     P = [p.astype(np.float64) for p in params[0]]
-    x = gen_x(cfg, 0).astype(np.float64)
-    dy = gen_dy(cfg, 0).astype(np.float64)
     shp = oracle.LayerShape(cfg.heads, cfg.causal, cfg.ln_eps)
-    t0 = time.perf_counter()
-    y, cache = oracle.layer_forward(x, P, shp)
-    dx, ws = oracle.layer_backward_input(dy, cache, P)
-    oracle.layer_backward_weight(ws)
-    dt = time.perf_counter() - t0
-    flops = sum(cfg.flops_per_layer())
+    dt, n = 0.0, 0
+    while dt < 10.0 and n < cfg.n_mb:
+        x = gen_x(cfg, n).astype(np.float64)
+        dy = gen_dy(cfg, n).astype(np.float64)
+        t0 = time.perf_counter()
+        y, cache = oracle.layer_forward(x, P, shp)
+        dx, ws = oracle.layer_backward_input(dy, cache, P)
+        oracle.layer_backward_weight(ws)
+        dt += time.perf_counter() - t0
+        n += 1
+    flops = n * sum(cfg.flops_per_layer())
     return {"value": round(flops / dt / 1e12, 4), "unit": "TFLOP/s", "cores": int(cores),
             "kind": "oracle",
-            "sample": (f"fp64 numpy oracle: F + B_input + B_weight of 1 of {cfg.layers} layers for 1 of "
+            "sample": (f"fp64 numpy oracle: F + B_input + B_weight of 1 of {cfg.layers} layers for {n} of "
                        f"{cfg.n_mb} micro-batches at full shape ({flops / 1e9:.0f} GFLOP algorithmic) "
                        f"in {dt:.1f} s")}
+
+
+def measured_traffic(cfg, kernel_class: str):
+    """HBM bytes per launch of a kernel class from the committed rocprofv3
+    counter summary of this workload (FETCH_SIZE + WRITE_SIZE, copy-calibrated),
+    or None when there is none or the kernel sources changed since."""
+    path = os.path.join(ROOT, "profiles", f"stage_{cfg.name}_kernels.md")
+    if not os.path.exists(path):
+        return None, "no counter summary for this workload"
+    txt = open(path).read()
+    try:
+        block = json.loads(txt.split("```json", 1)[1].split("```", 1)[0])
+    except (IndexError, ValueError):
+        return None, "counter summary unreadable"
+    from paper_2405_14009_amd.profile_summary import sources_digest
+    if block.get("sources_sha256") != sources_digest():
+        return None, "kernels changed since the counters were taken"
+    e = block.get("classes", {}).get(kernel_class, {})
+    if "bytes_per_dispatch" not in e:
+        return None, "no counter reading for this kernel class"
+    return e["bytes_per_dispatch"], os.path.relpath(path, ROOT)
 
 
 def main() -> int:
@@ -80,6 +105,9 @@ def main() -> int:
     ap.add_argument("--single-w", action="store_true",
                     help="one weight-pass call per micro-batch instead of merging consecutive "
                          "weight passes of the op list into one batched call")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run three plain 1 GiB device copies (calibrates the HBM byte "
+                         "counters of a profiler run) and exit")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the per-kernel events (for external profilers)")
     args = ap.parse_args()
@@ -101,6 +129,14 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("no HIP device", file=sys.stderr)
         return 1
+    if args.copy_probe:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copied 3 x 1 GiB")
+        return 0
     cfg = get_config(args.config)
     ops = op_list(cfg)
     log(f"workload {workload_name(cfg)}")
@@ -219,10 +255,11 @@ def main() -> int:
         dom = max(("gemm_fwd", "gemm_dgrad", "gemm_wgrad"), key=lambda n: prof[n]["ms"])
         r = prof[dom]
         achieved = r["flops"] / (r["ms"] / 1e3) / 1e12
+        traffic, tsrc = measured_traffic(cfg, dom)
         out["roofline"] = {"kernel": f"{dom} (bf16 MFMA GEMM)", "bound": "mfma",
                            "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                           "traffic": None,
+                           "traffic": traffic, "traffic_source": tsrc,
                            "avg_launch_us": round(1e3 * r["ms"] / r["launches"], 2),
                            "flops_per_launch": r["flops"] / r["launches"]}
     if not args.no_cpu_baseline:

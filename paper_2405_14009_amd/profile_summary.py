@@ -1,0 +1,196 @@
+"""Summarise rocprofv3 output of a stage benchmark run into a short markdown
+report with a machine-readable block that ``bench.py`` reads back.
+
+Inputs (CSV files written by ``rocprofv3 --output-format csv``):
+  --stats        ``*_kernel_stats.csv`` of ``rocprofv3 --kernel-trace --stats``
+  --fetch/--write ``*_counter_collection.csv`` of ``rocprofv3 --pmc FETCH_SIZE``
+                 and ``--pmc WRITE_SIZE`` runs of the same command
+  --copy-fetch/--copy-write  the same counters over ``bench.py --copy-probe``
+                 (plain 1 GiB device copies), which calibrate them: the
+                 factor is (bytes the copy must move) / (bytes the counter
+                 reports), applied to every kernel's reading.
+
+Kernel names map to the stage library's kernel classes (the same classes its
+per-launch profiler reports), so the per-launch averages here can be checked
+against the benchmark's own event timing.
+
+    python -m paper_2405_14009_amd.profile_summary --stats S.csv --fetch F.csv \\
+        --write W.csv --copy-fetch CF.csv --copy-write CW.csv --bench bench.json \\
+        --command "<commands>" --out profiles/<name>.md
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import json
+import os
+import re
+import sys
+from collections import defaultdict
+
+COPY_BYTES = 1 << 30  # per copy dispatch of bench.py --copy-probe (read and write)
+
+
+def sources_digest() -> str:
+    """sha256 over the kernel and runtime sources (name + content, sorted)."""
+    d = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(d)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            h.update(name.encode())
+            with open(os.path.join(d, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def kernel_class(name: str) -> str:
+    m = re.search(r"gemm_bf16_kernel<\s*\d+,\s*\d+,\s*\d+,\s*(true|false),\s*(true|false)", name)
+    if m:
+        return {("true", "false"): "gemm_fwd", ("true", "true"): "gemm_dgrad",
+                ("false", "false"): "gemm_wgrad"}.get(m.groups(), "gemm_other")
+    if "gemm_f32" in name:
+        return "gemm_f32"
+    if "attn_fwd_k" in name:
+        return "attn_fwd"
+    if "attn_bwd" in name or "attn_dot_k" in name:
+        return "attn_bwd"
+    if "ln_fwd_k" in name or "ln_bwd_k" in name:
+        return "layernorm"
+    if "colsum" in name:
+        return "reduce"
+    if "adamw" in name:
+        return "adamw"
+    if "softmax" in name:
+        return "softmax"
+    if "copyBuffer" in name or "copy" in name.lower():
+        return "copy"
+    return "other"
+
+
+def short(name: str) -> str:
+    name = name.replace("(anonymous namespace)::", "").replace("void ", "")
+    return name.split("(")[0] if "gemm" in name or "attn" in name else name[:90]
+
+
+def read_stats(path):
+    rows = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            rows.append({"name": r["Name"], "calls": int(r["Calls"]),
+                         "total_ns": float(r["TotalDurationNs"]), "avg_ns": float(r["AverageNs"])})
+    return rows
+
+
+def read_counter(path, counter):
+    """Per-dispatch values of one counter: list of (kernel name, value)."""
+    out = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] == counter:
+                out.append((r["Kernel_Name"], float(r["Counter_Value"])))
+    return out
+
+
+def calibrate(path, counter):
+    vals = [v for n, v in read_counter(path, counter) if kernel_class(n) == "copy" or "elementwise" in n]
+    vals = [v for v in vals if v > 0]
+    if not vals:
+        raise SystemExit(f"no copy dispatch with {counter} in {path}")
+    big = max(vals)
+    sel = [v for v in vals if v > 0.5 * big]  # the 1 GiB copies, not small helper launches
+    kib = sum(sel) / len(sel)
+    return COPY_BYTES / (kib * 1024.0), kib
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--stats", required=True)
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--copy-fetch")
+    ap.add_argument("--copy-write")
+    ap.add_argument("--bench", help="bench.py JSON line of the same build")
+    ap.add_argument("--command", required=True, help="the commands that produced the inputs")
+    ap.add_argument("--title", default="GPT-6.7B-shaped stage iteration")
+    ap.add_argument("--out", required=True)
+    a = ap.parse_args(argv)
+
+    stats = read_stats(a.stats)
+    tot = sum(r["total_ns"] for r in stats)
+    cls = defaultdict(lambda: {"calls": 0, "total_ns": 0.0})
+    for r in stats:
+        c = cls[kernel_class(r["name"])]
+        c["calls"] += r["calls"]
+        c["total_ns"] += r["total_ns"]
+
+    traffic = {}
+    cal = {}
+    if a.fetch and a.write and a.copy_fetch and a.copy_write:
+        ff, fk = calibrate(a.copy_fetch, "FETCH_SIZE")
+        fw, wk = calibrate(a.copy_write, "WRITE_SIZE")
+        cal = {"fetch_factor": round(ff, 4), "write_factor": round(fw, 4),
+               "copy_fetch_kib": round(fk, 1), "copy_write_kib": round(wk, 1),
+               "copy_bytes": COPY_BYTES}
+        acc = defaultdict(lambda: [0.0, 0.0, 0, 0])
+        for n, v in read_counter(a.fetch, "FETCH_SIZE"):
+            e = acc[kernel_class(n)]
+            e[0] += v * 1024.0 * ff
+            e[2] += 1
+        for n, v in read_counter(a.write, "WRITE_SIZE"):
+            e = acc[kernel_class(n)]
+            e[1] += v * 1024.0 * fw
+            e[3] += 1
+        for k, (fb, wb, nf, nw) in acc.items():
+            if nf and nw:
+                traffic[k] = {"fetch_bytes_per_dispatch": fb / nf, "write_bytes_per_dispatch": wb / nw,
+                              "bytes_per_dispatch": fb / nf + wb / nw}
+
+    bench = None
+    if a.bench:
+        with open(a.bench) as f:
+            for line in f:
+                line = line.strip()
+                if line.startswith("{"):
+                    bench = json.loads(line)
+
+    L = [f"# Kernel time and HBM traffic: {a.title}", ""]
+    L += ["Commands (from the repository root on one MI355X; `$R` is the repository path):", "", "```",
+          a.command.strip(), "```", ""]
+    L += ["| kernel class | dispatches | avg us / dispatch | % time | HBM bytes / dispatch (calibrated) |",
+          "|---|---:|---:|---:|---:|"]
+    for k, c in sorted(cls.items(), key=lambda kv: -kv[1]["total_ns"]):
+        t = traffic.get(k)
+        tb = f"{t['bytes_per_dispatch'] / 1e6:.1f} MB" if t else "—"
+        L.append(f"| {k} | {c['calls']} | {c['total_ns'] / c['calls'] / 1e3:.1f} | "
+                 f"{100 * c['total_ns'] / tot:.1f} | {tb} |")
+    L += ["", "Top kernels:", "", "| kernel | calls | avg us | % time |", "|---|---:|---:|---:|"]
+    for r in sorted(stats, key=lambda r: -r["total_ns"])[:14]:
+        L.append(f"| `{short(r['name'])}` | {r['calls']} | {r['avg_ns'] / 1e3:.1f} | "
+                 f"{100 * r['total_ns'] / tot:.2f} |")
+    if cal:
+        L += ["", f"Counter calibration (plain 1 GiB device copies): FETCH_SIZE reads "
+              f"{cal['copy_fetch_kib']:.0f} KiB and WRITE_SIZE {cal['copy_write_kib']:.0f} KiB per copy "
+              f"of {COPY_BYTES // 1024} KiB; factors {cal['fetch_factor']} (fetch) and "
+              f"{cal['write_factor']} (write) scale every reading above."]
+    if bench:
+        k = bench.get("kernels", {})
+        L += ["", f"bench.py line of the same build: value {bench['value']} {bench['unit']}, "
+              f"{bench.get('mb_per_s')} micro-batches/s; event-timed average per launch: " +
+              ", ".join(f"{n} {v['avg_us']} us" for n, v in k.items() if n.startswith("gemm"))]
+    block = {"sources_sha256": sources_digest(), "classes": {}, "calibration": cal}
+    for k, c in cls.items():
+        e = {"dispatches": c["calls"], "avg_us": round(c["total_ns"] / c["calls"] / 1e3, 2)}
+        if k in traffic:
+            e.update({kk: round(v) for kk, v in traffic[k].items()})
+        block["classes"][k] = e
+    L += ["", "Machine-readable (read by bench.py; `sources_sha256` is the digest of the kernel "
+          "sources these counters were taken with):", "", "```json", json.dumps(block, indent=1), "```", ""]
+    with open(a.out, "w") as f:
+        f.write("\n".join(L))
+    print(f"wrote {a.out}")
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
