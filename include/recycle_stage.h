@@ -92,7 +92,7 @@ typedef struct rc_mb {
   int32_t k;
 } rc_mb;
 
-enum { RC_OP_F = 0, RC_OP_B = 1, RC_OP_W = 2, RC_OP_STEP = 3 };
+enum { RC_OP_F = 0, RC_OP_B = 1, RC_OP_W = 2, RC_OP_STEP = 3, RC_OP_SKIP = 4, RC_OP_ROLLBACK = 5 };
 
 /* One op-log entry: the op 5-tuple (i=stage, j, k, c=op, k_s) plus the
  * sequence number and the stage-local iteration.  STEP has j = k = -1. */
@@ -203,6 +203,35 @@ rc_status rc_stage_backward_weight_many(rc_stage* st, const rc_mb* mbs, int32_t 
  * Errors: RC_ERR_BAD_STATE (a micro-batch of the iteration has not run W),
  *         RC_ERR_HIP. */
 rc_status rc_stage_optimizer_step(rc_stage* st, float grad_scale);
+
+/* Post-step local validation (section 5, the paragraph on bypassing optimizer
+ * synchronisation: each stage validates its own gradients after the
+ * all-reduce, steps on its own and its upstream stages' results, and rolls
+ * back when a downstream stage fails).
+ *
+ * rc_stage_grad_check: *sumsq = sum of squares of the finite entries of
+ * grad_scale * gradient, *nonfinite = number of NaN / Inf entries.  Reads the
+ * gradient being accumulated or, while the last call closed an iteration
+ * (step / skip / rollback), the gradient that iteration used; zero before
+ * the first weight pass of an iteration.  Fixed reduction order (bitwise
+ * reproducible).  Synchronises the handle's stream.
+ * Errors: RC_ERR_INVALID_ARG (NULL outputs; dry-run handle), RC_ERR_HIP. */
+rc_status rc_stage_grad_check(rc_stage* st, float grad_scale, double* sumsq, int64_t* nonfinite);
+
+/* Close the iteration without an update (a failed validation here or
+ * upstream): parameters, Adam state and the step count are unchanged; logs
+ * RC_OP_SKIP.  Errors: as rc_stage_optimizer_step. */
+rc_status rc_stage_optimizer_skip(rc_stage* st);
+
+/* Undo the optimizer step that was this handle's last call (a failed
+ * validation downstream).  AdamW is arithmetically reversible: p, m and v
+ * before the step are recomputed from their stepped values and the retained
+ * gradient, with no saved copy (fp32 rounding: relative error ~1e-7).  The
+ * step count goes back by one; the iteration stays closed; logs
+ * RC_OP_ROLLBACK with the undone step's iteration.
+ * Errors: RC_ERR_BAD_STATE (the last call was not a step, e.g. a second
+ * rollback, a skip, or any F/B/W or load_param after the step), RC_ERR_HIP. */
+rc_status rc_stage_optimizer_rollback(rc_stage* st);
 
 /* Copy up to cap op-log records into buf (may be NULL when cap == 0); *n
  * receives the total number of records. */

@@ -299,11 +299,29 @@ def adamw_update(p, g, m, v, t: int, hp: AdamHP, decay: bool):
     return p, m, v
 
 
+def adamw_rollback(p, g, m, v, t: int, hp: AdamHP, decay: bool):
+    """Undo the AdamW step number t: from the stepped (p, m, v) and the gradient g
+    that step used, the values before it.  No copy of the old state is needed
+    because every assignment of the step is invertible (section 5, post-step
+    validation paragraph: a rollback costs no extra memory for AdamW).
+
+    The assignments of ``adamw_update`` are undone in reverse order: the
+    parameter update used the new m and v, so p is restored first, then
+    v <- (v - (1-b2) g^2) / b2 and m <- (m - (1-b1) g) / b1."""
+    mhat = m / (1.0 - hp.beta1 ** t)
+    vhat = v / (1.0 - hp.beta2 ** t)
+    wd = hp.weight_decay if decay else 0.0
+    p = (p + hp.lr * mhat / (np.sqrt(vhat) + hp.eps)) / (1.0 - hp.lr * wd)
+    v = (v - (1.0 - hp.beta2) * g * g) / hp.beta2
+    m = (m - (1.0 - hp.beta1) * g) / hp.beta1
+    return p, m, v
+
+
 # ---------------------------------------------------------------------------
 # Stage object with the micro-batch state machine and op log
 # ---------------------------------------------------------------------------
 
-OP_F, OP_B, OP_W, OP_STEP = 0, 1, 2, 3
+OP_F, OP_B, OP_W, OP_STEP, OP_SKIP, OP_ROLLBACK = 0, 1, 2, 3, 4, 5
 MATRIX_IDS = (2, 4, 8, 10)
 
 
@@ -321,6 +339,11 @@ class OracleStage:
     Per micro-batch (j, k) and iteration: EMPTY -F-> F_DONE -B-> B_DONE -W->
     DONE.  B before F, W before B, F or B twice are BAD_STATE; the optimizer
     step is BAD_STATE while any micro-batch of the iteration is not DONE.
+    Post-step validation (section 5): ``grad_check`` reports the squared norm
+    and the non-finite entries of the gradient; ``optimizer_skip`` closes the
+    iteration without an update (a failed check here or upstream);
+    ``optimizer_rollback`` undoes the step just taken (a failed check
+    downstream), allowed only while no other call followed that step.
     ``max_stashed`` bounds micro-batches holding weight-pass intermediates
     (F..W), ``max_inflight`` those holding forward-only intermediates (F..B);
     exceeding either is OUT_OF_STASH.  Gradients are zeroed at the first W of
@@ -348,6 +371,8 @@ class OracleStage:
         self.wstash: Dict[Tuple[int, int], list] = {}
         self.grads_fresh = True
         self.log: List[Tuple[int, int, int, int, int, int]] = []
+        self.closed = False          # the last call closed an iteration (step / skip / rollback)
+        self.last_step_scale = None  # grad_scale of a step that may still be rolled back
 
     # -- bookkeeping -------------------------------------------------------
     def _record(self, op, mb):
@@ -371,6 +396,8 @@ class OracleStage:
         self.caches[mb] = caches
         self.state[mb] = "F"
         self._record(OP_F, mb)
+        self.closed = False
+        self.last_step_scale = None
         return y
 
     def backward_input(self, mb, dy):
@@ -381,6 +408,8 @@ class OracleStage:
         self.wstash[mb] = stashes
         self.state[mb] = "B"
         self._record(OP_B, mb)
+        self.closed = False
+        self.last_step_scale = None
         return dx
 
     def backward_weight(self, mb):
@@ -398,6 +427,8 @@ class OracleStage:
                 self.grads[l][p] += g
         self.state[mb] = "W"
         self._record(OP_W, mb)
+        self.closed = False
+        self.last_step_scale = None
 
     def optimizer_step(self, grad_scale: float = 1.0):
         pending = [mb for mb, s in self.state.items() if s != "W"]
@@ -417,3 +448,50 @@ class OracleStage:
         self.state.clear()
         self.grads_fresh = True
         self.iter += 1
+        self.closed = True
+        self.last_step_scale = grad_scale
+
+    def optimizer_skip(self):
+        """Close the iteration without an update."""
+        pending = [mb for mb, s in self.state.items() if s != "W"]
+        if pending:
+            raise StageError("BAD_STATE", f"optimizer skip with pending micro-batches {pending}")
+        if self.grads_fresh:
+            for layer in self.grads:
+                for g in layer:
+                    g[...] = 0.0
+        self._record(OP_SKIP, None)
+        self.state.clear()
+        self.grads_fresh = True
+        self.iter += 1
+        self.closed = True
+        self.last_step_scale = None
+
+    def optimizer_rollback(self):
+        """Undo the step just taken, from the retained gradients."""
+        if self.last_step_scale is None:
+            raise StageError("BAD_STATE", "rollback needs an optimizer step as the last call")
+        gs = self.last_step_scale
+        for l in range(len(self.params)):
+            for p in range(len(self.params[l])):
+                self.params[l][p], self.m[l][p], self.v[l][p] = adamw_rollback(
+                    self.params[l][p], gs * self.grads[l][p], self.m[l][p], self.v[l][p], self.t,
+                    self.hp, decay=p in MATRIX_IDS)
+        self.t -= 1
+        self.log.append((len(self.log), OP_ROLLBACK, -1, -1, self.pipeline_id, self.iter - 1))
+        self.last_step_scale = None
+
+    def grad_check(self, grad_scale: float = 1.0):
+        """(sum of squares, number of non-finite entries) of grad_scale * the
+        gradient: the one being accumulated, or, right after the iteration
+        closed, the one its step used (zero if no weight pass ran)."""
+        if self.grads_fresh and not self.closed:
+            return 0.0, 0
+        ss, bad = 0.0, 0
+        for layer in self.grads:
+            for g in layer:
+                x = grad_scale * g
+                fin = np.isfinite(x)
+                bad += int(x.size - fin.sum())
+                ss += float(np.sum(x[fin] ** 2))
+        return ss, bad

@@ -6,7 +6,8 @@ Python binding.
 """
 from ._lib import (  # noqa: F401
     BadStateError, HipError, InvalidArgError, OutOfStashError, RcError, UnsupportedError,
-    RC_OP_B, RC_OP_F, RC_OP_STEP, RC_OP_W, RC_READ_ADAM_M, RC_READ_ADAM_V, RC_READ_GRAD,
+    RC_OP_B, RC_OP_F, RC_OP_ROLLBACK, RC_OP_SKIP, RC_OP_STEP, RC_OP_W, RC_READ_ADAM_M,
+    RC_READ_ADAM_V, RC_READ_GRAD,
     RC_READ_PARAM, LIB_PATH, load,
 )
 from .stage import PARAM_NAMES, Stage, param_shape  # noqa: F401

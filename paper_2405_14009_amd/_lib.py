@@ -13,7 +13,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librecycle_
 RC_OK, RC_ERR_INVALID_ARG, RC_ERR_BAD_STATE, RC_ERR_OUT_OF_STASH, RC_ERR_HIP, RC_ERR_UNSUPPORTED = (
     0, -1, -2, -3, -4, -5)
 RC_FP32, RC_BF16 = 0, 1
-RC_OP_F, RC_OP_B, RC_OP_W, RC_OP_STEP = 0, 1, 2, 3
+RC_OP_F, RC_OP_B, RC_OP_W, RC_OP_STEP, RC_OP_SKIP, RC_OP_ROLLBACK = 0, 1, 2, 3, 4, 5
 RC_READ_PARAM, RC_READ_GRAD, RC_READ_ADAM_M, RC_READ_ADAM_V = 0, 1, 2, 3
 RC_NUM_PARAMS = 12
 
@@ -21,7 +21,8 @@ RC_NUM_PARAMS = 12
 EXPORTED = (
     "rc_stage_memory_requirements", "rc_stage_create", "rc_stage_destroy", "rc_stage_load_param",
     "rc_stage_read", "rc_stage_forward", "rc_stage_backward_input", "rc_stage_backward_weight",
-    "rc_stage_backward_weight_many", "rc_stage_optimizer_step", "rc_stage_op_log",
+    "rc_stage_backward_weight_many", "rc_stage_optimizer_step", "rc_stage_grad_check",
+    "rc_stage_optimizer_skip", "rc_stage_optimizer_rollback", "rc_stage_op_log",
     "rc_stage_stash_usage", "rc_stage_set_stream",
     "rc_stage_synchronize", "rc_stage_profile_enable", "rc_stage_profile_read", "rc_last_error",
 )
@@ -104,6 +105,9 @@ def load() -> ctypes.CDLL:
         "rc_stage_backward_weight": [P, RcMb],
         "rc_stage_backward_weight_many": [P, ctypes.POINTER(RcMb), I32],
         "rc_stage_optimizer_step": [P, F32],
+        "rc_stage_grad_check": [P, F32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
+        "rc_stage_optimizer_skip": [P],
+        "rc_stage_optimizer_rollback": [P],
         "rc_stage_op_log": [P, ctypes.POINTER(RcOpRecord), I32, ctypes.POINTER(I32)],
         "rc_stage_stash_usage": [P, ctypes.POINTER(I32), ctypes.POINTER(I32)],
         "rc_stage_set_stream": [P, P],

@@ -44,6 +44,79 @@ __global__ __launch_bounds__(NT) void adamw_k(float4* __restrict__ p, const floa
   }
 }
 
+// Inverse of adam_one for the same step: the stepped p, m, v and the gradient
+// of that step give the values before it (each assignment undone in reverse
+// order; v is clamped at zero against rounding).
+__device__ __forceinline__ float adam_undo(float p, float g, float& m, float& v, bool decay,
+                                           float lr, float b1, float b2, float eps, float wd,
+                                           float step_size, float inv_sqrt_bc2, float gs) {
+  g *= gs;
+  p += step_size * m / (sqrtf(v) * inv_sqrt_bc2 + eps);
+  if (decay) p /= (1.f - lr * wd);
+  v = fmaxf((v - (1.f - b2) * g * g) / b2, 0.f);
+  m = (m - (1.f - b1) * g) / b1;
+  return p;
+}
+
+__global__ __launch_bounds__(NT) void adamw_undo_k(float4* __restrict__ p, const float4* __restrict__ g,
+                                                   float4* __restrict__ m, float4* __restrict__ v,
+                                                   bf16* __restrict__ wb, long n4, long nd4, float lr,
+                                                   float b1, float b2, float eps, float wd,
+                                                   float step_size, float inv_sqrt_bc2, float gs) {
+  for (long i = blockIdx.x * (long)NT + threadIdx.x; i < n4; i += (long)gridDim.x * NT) {
+    float4 pp = p[i], gg = g[i], mm = m[i], vv = v[i];
+    const bool dec = i < nd4;
+    pp.x = adam_undo(pp.x, gg.x, mm.x, vv.x, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
+    pp.y = adam_undo(pp.y, gg.y, mm.y, vv.y, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
+    pp.z = adam_undo(pp.z, gg.z, mm.z, vv.z, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
+    pp.w = adam_undo(pp.w, gg.w, mm.w, vv.w, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
+    p[i] = pp;
+    m[i] = mm;
+    v[i] = vv;
+    if (wb != nullptr && dec) {
+      bf16* o = wb + 4 * i;
+      o[0] = (bf16)pp.x;
+      o[1] = (bf16)pp.y;
+      o[2] = (bf16)pp.z;
+      o[3] = (bf16)pp.w;
+    }
+  }
+}
+
+// Per-block partial sum of squares of the finite entries of gs * g and count
+// of non-finite entries; a fixed grid and fixed reduction order make the
+// result bitwise reproducible.
+__global__ __launch_bounds__(NT) void grad_check_k(const float4* __restrict__ g, long n4, float gs,
+                                                   float* __restrict__ part, int* __restrict__ bad) {
+  __shared__ float red[NT / 64];
+  __shared__ int redi[NT / 64];
+  float s = 0.f;
+  int nb = 0;
+  for (long i = blockIdx.x * (long)NT + threadIdx.x; i < n4; i += (long)gridDim.x * NT) {
+    const float4 v = g[i];
+    const float e[4] = {gs * v.x, gs * v.y, gs * v.z, gs * v.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (isfinite(e[k]))
+        s += e[k] * e[k];
+      else
+        ++nb;
+    }
+  }
+  const float tot = block_sum<NT>(s, red);
+  int c = nb;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+  if ((threadIdx.x & 63) == 0) redi[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int t = 0;
+    for (int w = 0; w < NT / 64; ++w) t += redi[w];
+    part[blockIdx.x] = tot;
+    bad[blockIdx.x] = t;
+  }
+}
+
 __global__ __launch_bounds__(NT) void cast_k(const float* __restrict__ s, bf16* __restrict__ d, long n) {
   for (long i = blockIdx.x * (long)NT + threadIdx.x; i < n; i += (long)gridDim.x * NT) d[i] = (bf16)s[i];
 }
@@ -67,6 +140,24 @@ hipError_t adamw_step(float* p, const float* g, float* m, float* v, void* wb, lo
   hipLaunchKernelGGL(adamw_k, dim3(grid_for(n / 4)), dim3(NT), 0, s, (float4*)p, (const float4*)g,
                      (float4*)m, (float4*)v, (bf16*)wb, n / 4, n_decay / 4, lr, beta1, beta2, eps,
                      wd, step_size, inv_sqrt_bc2, grad_scale);
+  return hipGetLastError();
+}
+
+hipError_t adamw_undo(float* p, const float* g, float* m, float* v, void* wb, long n, long n_decay,
+                      float lr, float beta1, float beta2, float eps, float wd, float step_size,
+                      float inv_sqrt_bc2, float grad_scale, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if ((n & 3) || (n_decay & 3)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(adamw_undo_k, dim3(grid_for(n / 4)), dim3(NT), 0, s, (float4*)p, (const float4*)g,
+                     (float4*)m, (float4*)v, (bf16*)wb, n / 4, n_decay / 4, lr, beta1, beta2, eps,
+                     wd, step_size, inv_sqrt_bc2, grad_scale);
+  return hipGetLastError();
+}
+
+hipError_t grad_check(const float* g, long n, float grad_scale, float* part, int* bad, hipStream_t s) {
+  if (n <= 0 || (n & 3)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(grad_check_k, dim3(GRAD_CHECK_BLOCKS), dim3(NT), 0, s, (const float4*)g, n / 4,
+                     grad_scale, part, bad);
   return hipGetLastError();
 }
 

@@ -61,5 +61,16 @@ hipError_t adamw_step(float* p, const float* g, float* m, float* v, void* wb, lo
                       float lr, float beta1, float beta2, float eps, float wd, float step_size,
                       float inv_sqrt_bc2, float grad_scale, hipStream_t s);
 
+// Inverse of adamw_step for the same step number and gradient (rollback).
+hipError_t adamw_undo(float* p, const float* g, float* m, float* v, void* wb, long n, long n_decay,
+                      float lr, float beta1, float beta2, float eps, float wd, float step_size,
+                      float inv_sqrt_bc2, float grad_scale, hipStream_t s);
+
+// Per-block partials over n fp32 gradients (n % 4 == 0): part[b] = sum of
+// squares of the finite entries of grad_scale * g, bad[b] = non-finite count,
+// for b < GRAD_CHECK_BLOCKS.
+constexpr int GRAD_CHECK_BLOCKS = 1024;
+hipError_t grad_check(const float* g, long n, float grad_scale, float* part, int* bad, hipStream_t s);
+
 hipError_t cast_f32_to_bf16(const float* src, void* dst, long n, hipStream_t s);
 hipError_t fill_f32(float* dst, long n, float value, hipStream_t s);

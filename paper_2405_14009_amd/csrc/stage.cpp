@@ -75,7 +75,7 @@ struct Layout {
   WLayer w;
   FLayer fl;
   size_t wslot_bytes, fslot_bytes, off_fslots, stash_bytes;
-  size_t off_S, off_dS, off_dO, off_dv, off_part, work_bytes;
+  size_t off_S, off_dS, off_dO, off_dv, off_check, off_part, work_bytes;
 };
 
 rc_status make_layout(const rc_stage_config* c, Layout& y) {
@@ -172,6 +172,7 @@ rc_status make_layout(const rc_stage_config* c, Layout& y) {
   y.off_dS = take(y.flash ? 0 : ss * E);
   y.off_dO = take(T * h * E);
   y.off_dv = take(y.flash ? rows * 4 : 0);
+  y.off_check = take(8 * GRAD_CHECK_BLOCKS);
   y.off_part = take(4 * colsum_part_floats(y.T, (int)std::max(3 * h, f),
                                            std::min(y.wslots, (int)GEMM_MAX_SEG)));
   y.work_bytes = o;
@@ -198,6 +199,10 @@ struct rc_stage {
   std::vector<rc_op_record> log;
   int64_t iter = 0, t = 0;
   bool grads_fresh = true;
+  // Post-step validation: `closed` = the last call closed an iteration (step,
+  // skip, rollback); a step can be rolled back while it is the last call.
+  bool closed = false, can_rollback = false;
+  float last_scale = 1.f;
   // per-kernel profile
   struct Rec {
     int kind;
@@ -587,6 +592,23 @@ rc_status run_optimizer(rc_stage* st, float grad_scale) {
   return RC_OK;
 }
 
+// Undo the step number st->t with the gradients it used (still in the
+// gradient buffer: the next iteration's first weight pass overwrites them).
+rc_status run_rollback(rc_stage* st) {
+  const Layout& y = st->lay;
+  const double t = (double)st->t;
+  const rc_adam_config& a = st->adam;
+  const double bc1 = 1.0 - std::pow((double)a.beta1, t);
+  const double bc2 = 1.0 - std::pow((double)a.beta2, t);
+  Prof pr(st, RC_K_ADAM, 0, 28.0 * y.n_total + (y.bf ? 2.0 * y.n_mat : 0.0));
+  HIPCHK(adamw_undo((float*)(st->state + y.off_master), (const float*)(st->state + y.off_grad),
+                    (float*)(st->state + y.off_m), (float*)(st->state + y.off_v),
+                    y.bf ? (void*)(st->state + y.off_wb) : nullptr, y.n_total, y.n_mat, a.lr, a.beta1,
+                    a.beta2, a.eps, a.weight_decay, (float)(a.lr / bc1), (float)(1.0 / std::sqrt(bc2)),
+                    st->last_scale, st->stream));
+  return RC_OK;
+}
+
 void record(rc_stage* st, int op, int j, int k) {
   rc_op_record r;
   r.seq = (int64_t)st->log.size();
@@ -697,6 +719,7 @@ rc_status rc_stage_load_param(rc_stage* st, int32_t layer, int32_t param_id, con
   if (st->lay.bf && matrix)
     HIPCHK(cast_f32_to_bf16(dst, (char*)st->state + st->lay.off_wb + 2 * p.off, p.count, st->stream));
   HIPCHK(hipStreamSynchronize(st->stream));
+  st->can_rollback = false;  // the step's inverse no longer applies to replaced values
   return RC_OK;
 }
 
@@ -740,6 +763,8 @@ rc_status rc_stage_forward(rc_stage* st, rc_mb mb, const void* x, void* y) {
   }
   st->mbs[key] = {1, ws, fs};
   record(st, RC_OP_F, mb.j, mb.k);
+  st->closed = false;
+  st->can_rollback = false;
   return RC_OK;
 }
 
@@ -758,6 +783,8 @@ rc_status rc_stage_backward_input(rc_stage* st, rc_mb mb, const void* dy, void* 
   it->second.fs = -1;
   it->second.state = 2;
   record(st, RC_OP_B, mb.j, mb.k);
+  st->closed = false;
+  st->can_rollback = false;
   return RC_OK;
 }
 
@@ -789,6 +816,8 @@ rc_status rc_stage_backward_weight_many(rc_stage* st, const rc_mb* mbs, int32_t 
     m.ws = -1;
     m.state = 3;
     record(st, RC_OP_W, mbs[q].j, mbs[q].k);
+    st->closed = false;
+    st->can_rollback = false;
   }
   st->grads_fresh = false;
   return RC_OK;
@@ -812,6 +841,68 @@ rc_status rc_stage_optimizer_step(rc_stage* st, float grad_scale) {
   st->mbs.clear();
   st->grads_fresh = true;
   st->iter += 1;
+  st->closed = true;
+  st->can_rollback = true;
+  st->last_scale = grad_scale;
+  return RC_OK;
+}
+
+rc_status rc_stage_optimizer_skip(rc_stage* st) {
+  if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
+  for (auto& kv : st->mbs)
+    if (kv.second.state != 3)
+      return fail(RC_ERR_BAD_STATE, "optimizer skip while micro-batch (" +
+                                        std::to_string(kv.first.first) + "," +
+                                        std::to_string(kv.first.second) + ") has not run W");
+  // the gradient of an iteration without a weight pass is zero (as a step would use it)
+  if (!st->dry && st->grads_fresh)
+    HIPCHK(fill_f32((float*)(st->state + st->lay.off_grad), st->lay.n_total, 0.f, st->stream));
+  record(st, RC_OP_SKIP, -1, -1);
+  st->mbs.clear();
+  st->grads_fresh = true;
+  st->iter += 1;
+  st->closed = true;
+  st->can_rollback = false;
+  return RC_OK;
+}
+
+rc_status rc_stage_optimizer_rollback(rc_stage* st) {
+  if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
+  if (!st->can_rollback) return fail(RC_ERR_BAD_STATE, "rollback needs an optimizer step as the last call");
+  if (!st->dry) {
+    rc_status r = run_rollback(st);
+    if (r != RC_OK) return r;
+  }
+  st->t -= 1;
+  record(st, RC_OP_ROLLBACK, -1, -1);
+  st->log.back().iter = st->iter - 1;  // the iteration whose step is undone
+  st->can_rollback = false;
+  return RC_OK;
+}
+
+rc_status rc_stage_grad_check(rc_stage* st, float grad_scale, double* sumsq, int64_t* nonfinite) {
+  if (!st || !sumsq || !nonfinite) return fail(RC_ERR_INVALID_ARG, "bad grad_check arguments");
+  *sumsq = 0.0;
+  *nonfinite = 0;
+  if (st->grads_fresh && !st->closed) return RC_OK;  // no weight pass yet: zero gradient
+  if (st->dry) return fail(RC_ERR_INVALID_ARG, "dry-run handle has no device memory");
+  const Layout& y = st->lay;
+  float* part = (float*)(st->work + y.off_check);
+  int* bad = (int*)(part + GRAD_CHECK_BLOCKS);
+  HIPCHK(grad_check((const float*)(st->state + y.off_grad), y.n_total, grad_scale, part, bad, st->stream));
+  std::vector<float> hp(GRAD_CHECK_BLOCKS);
+  std::vector<int> hb(GRAD_CHECK_BLOCKS);
+  HIPCHK(hipMemcpyAsync(hp.data(), part, 4 * GRAD_CHECK_BLOCKS, hipMemcpyDeviceToHost, st->stream));
+  HIPCHK(hipMemcpyAsync(hb.data(), bad, 4 * GRAD_CHECK_BLOCKS, hipMemcpyDeviceToHost, st->stream));
+  HIPCHK(hipStreamSynchronize(st->stream));
+  double s = 0.0;
+  int64_t b = 0;
+  for (int i = 0; i < GRAD_CHECK_BLOCKS; ++i) {
+    s += hp[i];
+    b += hb[i];
+  }
+  *sumsq = s;
+  *nonfinite = b;
   return RC_OK;
 }
 

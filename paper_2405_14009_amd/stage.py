@@ -157,6 +157,22 @@ class Stage:
         """This stage's AdamW step (no cross-stage synchronisation)."""
         L.check(self._lib.rc_stage_optimizer_step(self._h, float(grad_scale)))
 
+    def grad_check(self, grad_scale: float = 1.0):
+        """Post-step local validation: (sum of squares, non-finite count) of
+        grad_scale * the gradient."""
+        ss, bad = ctypes.c_double(), ctypes.c_int64()
+        L.check(self._lib.rc_stage_grad_check(self._h, float(grad_scale), ctypes.byref(ss),
+                                              ctypes.byref(bad)))
+        return ss.value, bad.value
+
+    def optimizer_skip(self) -> None:
+        """Close the iteration without an update."""
+        L.check(self._lib.rc_stage_optimizer_skip(self._h))
+
+    def optimizer_rollback(self) -> None:
+        """Undo the optimizer step that was the last call."""
+        L.check(self._lib.rc_stage_optimizer_rollback(self._h))
+
     # -- state access -----------------------------------------------------------
     def load_param(self, layer: int, pid: int, value) -> None:
         a = np.ascontiguousarray(value, dtype=np.float32)

@@ -210,6 +210,39 @@ def test_dry_run_batched_weight_pass_errors_are_all_or_nothing():
         st.backward_weight_many([MB(0)])
 
 
+def test_dry_run_skip_and_rollback_rules_match_oracle():
+    """Post-step validation calls: the same accept / refuse decisions and op
+    log as the oracle over a sequence that exercises every rule."""
+    lib_or_skip()
+    import paper_2405_14009_amd as P
+    cfg = get_config("tiny").with_(n_mb=2, max_stashed_mb=2, max_inflight_mb=2)
+    st = P.Stage.from_config(cfg, dry_run=True)
+    o = oracle.OracleStage(cfg.with_(layers=0), [])
+    z = np.zeros((1, 1, 1))
+    m0, m1 = MB(0), MB(1)
+    seq = [("ROLLBACK", None), ("F", m0), ("SKIP", None), ("B", m0), ("W", m0), ("SKIP", None),
+           ("ROLLBACK", None), ("F", m0), ("B", m0), ("W", m0), ("STEP", None), ("ROLLBACK", None),
+           ("ROLLBACK", None), ("STEP", None), ("ROLLBACK", None), ("STEP", None), ("F", m1),
+           ("ROLLBACK", None), ("B", m1), ("W", m1), ("STEP", None), ("SKIP", None),
+           ("ROLLBACK", None)]
+    for kind, mb in seq:
+        got = want = "OK"
+        try:
+            {"F": lambda: st.forward(mb), "B": lambda: st.backward_input(mb),
+             "W": lambda: st.backward_weight(mb), "STEP": st.optimizer_step,
+             "SKIP": st.optimizer_skip, "ROLLBACK": st.optimizer_rollback}[kind]()
+        except P.BadStateError:
+            got = "BAD_STATE"
+        try:
+            {"F": lambda: o.forward(mb, z), "B": lambda: o.backward_input(mb, z),
+             "W": lambda: o.backward_weight(mb), "STEP": o.optimizer_step,
+             "SKIP": o.optimizer_skip, "ROLLBACK": o.optimizer_rollback}[kind]()
+        except oracle.StageError as e:
+            want = e.code
+        assert got == want, (kind, mb)
+    assert st.op_log() == [tuple(r) for r in o.log]
+
+
 def test_product_fails_loudly_without_gpu():
     lib_or_skip()
     import torch

@@ -1,0 +1,161 @@
+"""Post-step validation on the GPU (section 5): gradient check, optimizer skip
+and AdamW rollback, through the C ABI, against the fp64 oracle."""
+import numpy as np
+import pytest
+
+import oracle
+from synth import MB, gen_dy, gen_params, gen_x, get_config, op_list
+from tests.conftest import rel_l2
+from tests.gpu_harness import log, run_gpu, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    import paper_2405_14009_amd  # noqa: F401
+    yield
+
+
+def _iteration(cfg):
+    return op_list(cfg, with_step=False)
+
+
+def _state(stage):
+    from paper_2405_14009_amd import RC_READ_ADAM_M, RC_READ_ADAM_V, RC_READ_PARAM
+    return (stage.read_all(RC_READ_PARAM), stage.read_all(RC_READ_ADAM_M),
+            stage.read_all(RC_READ_ADAM_V))
+
+
+def _close(a, b, tol):
+    for la, lb in zip(a, b):
+        for x, y in zip(la, lb):
+            if np.linalg.norm(y) == 0:
+                assert np.abs(x).max() <= tol * 1e-3, np.abs(x).max()
+            else:
+                assert rel_l2(x, y) <= tol, rel_l2(x, y)
+
+
+@pytest.mark.parametrize("name", ["small_f32", "small_bf16"])
+def test_rollback_restores_the_state_before_the_step(name):
+    cfg = get_config(name)
+    log(f"[rollback] {name}")
+    from paper_2405_14009_amd import Stage
+    st = Stage.from_config(cfg)
+    st.load_params(gen_params(cfg))
+    run_gpu(cfg, _iteration(cfg), stage=st, read_state=False, keep_outputs=False)
+    st.optimizer_step()                      # t = 1
+    ops2 = _iteration(cfg)
+    run_gpu(cfg, ops2, stage=st, read_state=False, keep_outputs=False)
+    before = _state(st)
+    x0 = to_device(gen_x(cfg, 0), cfg.dtype)
+    st.optimizer_step(grad_scale=0.5)        # t = 2
+    stepped = _state(st)
+    st.optimizer_rollback()
+    after = _state(st)
+    _close(after[0], before[0], 1e-6)        # parameters: fp32 rounding of the inverse
+    _close(after[1], before[1], 1e-5)
+    _close(after[2], before[2], 1e-5)
+    st.forward(MB(0), x0)                    # next iteration runs on the restored weights
+    with pytest.raises(Exception):
+        st.optimizer_rollback()              # nothing to undo any more
+    log(f"[rollback] {name}: restored within tolerance; step moved params by "
+        f"{max(rel_l2(s, b) for ls, lb in zip(stepped[0], before[0]) for s, b in zip(ls, lb)):.2e}")
+    st.close()
+
+
+def test_rollback_then_step_equals_step():
+    cfg = get_config("small_bf16")
+    from paper_2405_14009_amd import Stage
+    st = Stage.from_config(cfg)
+    st.load_params(gen_params(cfg))
+    run_gpu(cfg, _iteration(cfg), stage=st, read_state=False, keep_outputs=False)
+    st.optimizer_step()
+    once = _state(st)
+    st.optimizer_rollback()
+    st.optimizer_step()  # same gradient, same step number
+    again = _state(st)
+    _close(again[0], once[0], 1e-6)
+    _close(again[1], once[1], 1e-5)
+    _close(again[2], once[2], 1e-5)
+    st.close()
+
+
+def test_skip_leaves_parameters_and_step_count():
+    cfg = get_config("small_f32")
+    from paper_2405_14009_amd import Stage
+    st = Stage.from_config(cfg)
+    st.load_params(gen_params(cfg))
+    before = _state(st)
+    run_gpu(cfg, _iteration(cfg), stage=st, read_state=False, keep_outputs=False)
+    st.optimizer_skip()
+    after = _state(st)
+    for la, lb in zip(after, before):
+        for x, y in zip(la, lb):
+            for u, v in zip(x, y):
+                assert np.array_equal(u, v)
+    # the next step is still step 1: same result as the oracle's first step
+    g = run_gpu(cfg, _iteration(cfg) + [op_list(cfg)[-1]], stage=st, read_state=True, keep_outputs=False)
+    o = oracle.run_oplist(cfg)
+    for l in range(cfg.layers):
+        for p in range(12):
+            assert rel_l2(g.params[l][p], o.stage.params[l][p]) < 1e-5
+    st.close()
+
+
+@pytest.mark.parametrize("name", ["small_f32", "small_bf16"])
+def test_grad_check_against_oracle(name):
+    cfg = get_config(name)
+    from paper_2405_14009_amd import Stage
+    st = Stage.from_config(cfg)
+    st.load_params(gen_params(cfg))
+    assert st.grad_check() == (0.0, 0)
+    run_gpu(cfg, _iteration(cfg), stage=st, read_state=False, keep_outputs=False)
+    o = oracle.OracleStage(cfg, gen_params(cfg))
+    for op in _iteration(cfg):
+        if op.kind == "F":
+            o.forward(op.mb, gen_x(cfg, op.mb.j, op.mb.k))
+        elif op.kind == "B":
+            o.backward_input(op.mb, gen_dy(cfg, op.mb.j, op.mb.k))
+        else:
+            o.backward_weight(op.mb)
+    ss, bad = st.grad_check(0.5)
+    ss_o, bad_o = o.grad_check(0.5)
+    tol = 2e-5 if cfg.dtype == "f32" else 4e-2
+    log(f"[grad_check] {name}: gpu {ss:.6e} oracle {ss_o:.6e}")
+    assert bad == 0 and bad_o == 0 and abs(ss - ss_o) <= tol * ss_o
+    assert st.grad_check(0.5) == (ss, bad)   # bitwise reproducible
+    st.optimizer_step()
+    assert st.grad_check(0.5) == (ss, bad)   # right after the step: the gradient it used
+    st.close()
+
+
+def test_grad_check_counts_nonfinite_and_skip_keeps_weights():
+    cfg = get_config("small_f32").with_(n_mb=1, schedule="coupled")
+    from paper_2405_14009_amd import Stage
+    st = Stage.from_config(cfg)
+    st.load_params(gen_params(cfg))
+    before = _state(st)
+    dy = gen_dy(cfg, 0).copy()
+    dy[0, 3, 5] = np.nan
+    x = to_device(gen_x(cfg, 0), cfg.dtype)
+    st.forward(MB(0), x)
+    st.backward_input(MB(0), to_device(dy, cfg.dtype))
+    st.backward_weight(MB(0))
+    ss, bad = st.grad_check()
+    o = oracle.OracleStage(cfg, gen_params(cfg))
+    o.forward(MB(0), gen_x(cfg, 0))
+    o.backward_input(MB(0), dy)
+    o.backward_weight(MB(0))
+    ss_o, bad_o = o.grad_check()
+    log(f"[grad_check] planted NaN: gpu {bad} non-finite, oracle {bad_o}")
+    assert bad > 0 and bad_o > 0
+    st.optimizer_skip()
+    after = _state(st)
+    for x1, y1 in zip(after[0], before[0]):
+        for u, v in zip(x1, y1):
+            assert np.array_equal(u, v)
+    st.close()

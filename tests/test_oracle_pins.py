@@ -476,6 +476,120 @@ def test_stage_step_uses_decay_only_on_matrices():
 
 
 # ---------------------------------------------------------------------------
+# Post-step validation, skip and rollback (section 5)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("decay", [True, False])
+def test_adamw_rollback_inverts_the_step(decay):
+    """Round trip at several step numbers: rollback(step(p, m, v)) == (p, m, v)."""
+    rng = np.random.default_rng(7)
+    hp = ost.AdamHP()
+    for t in (1, 2, 7, 40):
+        p = rng.standard_normal(500) * 0.02
+        m = rng.standard_normal(500) * 1e-3 if t > 1 else np.zeros(500)
+        v = rng.random(500) * 1e-6 if t > 1 else np.zeros(500)
+        g = rng.standard_normal(500) * 1e-3
+        p1, m1, v1 = ost.adamw_update(p, g, m, v, t, hp, decay=decay)
+        p0, m0, v0 = ost.adamw_rollback(p1, g, m1, v1, t, hp, decay=decay)
+        assert rel_l2(p0, p) < 1e-12
+        assert np.abs(m0 - m).max() <= 1e-12 * max(np.abs(g).max(), np.abs(m).max())
+        assert np.abs(v0 - v).max() <= 1e-12 * max((g * g).max(), np.abs(v).max())
+        # undoing step t with the bias correction of another step number is not an inverse
+        pw, _, _ = ost.adamw_rollback(p1, g, m1, v1, t + 1, hp, decay=decay)
+        assert rel_l2(pw, p) > 1e-6
+
+
+def test_adamw_rollback_against_torch_optim_history():
+    """Two torch AdamW steps then one rollback land on torch's one-step state."""
+    torch = pytest.importorskip("torch")
+    hp = ost.AdamHP()
+    rng = np.random.default_rng(3)
+    p0 = rng.standard_normal(300) * 0.02
+    g1, g2 = rng.standard_normal(300) * 1e-3, rng.standard_normal(300) * 1e-3
+    tp = torch.nn.Parameter(torch.tensor(p0, dtype=torch.float64))
+    opt = torch.optim.AdamW([tp], lr=hp.lr, betas=(hp.beta1, hp.beta2), eps=hp.eps,
+                            weight_decay=hp.weight_decay)
+    tp.grad = torch.tensor(g1, dtype=torch.float64)
+    opt.step()
+    after1 = tp.detach().numpy().copy()
+    st = opt.state[tp]
+    m_1, v_1 = st["exp_avg"].numpy().copy(), st["exp_avg_sq"].numpy().copy()
+    tp.grad = torch.tensor(g2, dtype=torch.float64)
+    opt.step()
+    p, m, v = ost.adamw_rollback(tp.detach().numpy(), g2, st["exp_avg"].numpy(),
+                                 st["exp_avg_sq"].numpy(), 2, hp, decay=True)
+    assert rel_l2(p, after1) < 1e-12 and rel_l2(m, m_1) < 1e-10 and rel_l2(v, v_1) < 1e-10
+
+
+def _stage_after_iteration(cfg):
+    st = oracle.OracleStage(cfg, gen_params(cfg))
+    for op in op_list(cfg, with_step=False):
+        if op.kind == "F":
+            st.forward(op.mb, gen_x(cfg, op.mb.j, op.mb.k))
+        elif op.kind == "B":
+            st.backward_input(op.mb, gen_dy(cfg, op.mb.j, op.mb.k))
+        else:
+            st.backward_weight(op.mb)
+    return st
+
+
+def test_stage_skip_and_rollback_rules():
+    cfg = small_cfg(layers=1, n_mb=2)
+    st = _stage_after_iteration(cfg)
+    before = copy.deepcopy((st.params, st.m, st.v, st.t))
+    st.optimizer_skip()
+    assert st.t == before[3] and st.iter == 1
+    for l in range(cfg.layers):
+        for p in range(12):
+            assert np.array_equal(st.params[l][p], before[0][l][p])
+    with pytest.raises(oracle.StageError):          # nothing to undo after a skip
+        st.optimizer_rollback()
+    # a step, then its rollback: back to the state before the step
+    st2 = _stage_after_iteration(cfg)
+    st2.optimizer_step(grad_scale=0.5)
+    st2.optimizer_rollback()
+    assert st2.t == 0
+    for l in range(cfg.layers):
+        for p in range(12):
+            assert rel_l2(st2.params[l][p], before[0][l][p]) < 1e-12
+            assert np.abs(st2.m[l][p]).max() < 1e-15 and np.abs(st2.v[l][p]).max() < 1e-20
+    with pytest.raises(oracle.StageError):          # only once
+        st2.optimizer_rollback()
+    # after any call that follows the step, its rollback is refused
+    st3 = _stage_after_iteration(cfg)
+    st3.optimizer_step()
+    st3.forward(MB(0), gen_x(cfg, 0))
+    with pytest.raises(oracle.StageError):
+        st3.optimizer_rollback()
+    assert [r[1] for r in st2.log[-2:]] == [ost.OP_STEP, ost.OP_ROLLBACK]
+    assert st2.log[-1][5] == st2.log[-2][5]          # the rollback belongs to the stepped iteration
+
+
+def test_grad_check_matches_fused_gradient_norm():
+    """The squared norm reported equals that of the fused reverse pass's
+    gradient (an independent path), and planted non-finite entries are counted."""
+    cfg = small_cfg(layers=2, n_mb=2)
+    st = _stage_after_iteration(cfg)
+    params = params64(cfg)
+    shp = shape_of(cfg)
+    total = None
+    for mb in (MB(0), MB(1)):
+        x = gen_x(cfg, mb.j, mb.k).astype(F64)
+        y, caches = ost.stage_forward(x, params, shp)
+        _, g = ost.stage_backward_fused(gen_dy(cfg, mb.j, mb.k).astype(F64), caches, params)
+        total = g if total is None else [[a + b for a, b in zip(la, lb)] for la, lb in zip(total, g)]
+    ref = sum(float(np.sum((0.5 * t) ** 2)) for layer in total for t in layer)
+    ss, bad = st.grad_check(grad_scale=0.5)
+    assert bad == 0 and abs(ss - ref) <= 1e-12 * ref
+    st.grads[0][2][0, 0] = np.nan
+    st.grads[1][9][3] = np.inf
+    ss2, bad2 = st.grad_check()
+    assert bad2 == 2 and np.isfinite(ss2)
+    fresh = oracle.OracleStage(cfg, gen_params(cfg))
+    assert fresh.grad_check() == (0.0, 0)
+
+
+# ---------------------------------------------------------------------------
 # Mutation checks: a planted mistake in the oracle must fail a pin
 # ---------------------------------------------------------------------------
 
