@@ -312,6 +312,8 @@ def adamw_rollback(p, g, m, v, t: int, hp: AdamHP, decay: bool):
     vhat = v / (1.0 - hp.beta2 ** t)
     wd = hp.weight_decay if decay else 0.0
     p = (p + hp.lr * mhat / (np.sqrt(vhat) + hp.eps)) / (1.0 - hp.lr * wd)
+    if t == 1:  # the moments before the first step are the zero initial state
+        return p, np.zeros_like(m), np.zeros_like(v)
     v = (v - (1.0 - hp.beta2) * g * g) / hp.beta2
     m = (m - (1.0 - hp.beta1) * g) / hp.beta1
     return p, m, v

@@ -46,15 +46,17 @@ __global__ __launch_bounds__(NT) void adamw_k(float4* __restrict__ p, const floa
 
 // Inverse of adam_one for the same step: the stepped p, m, v and the gradient
 // of that step give the values before it (each assignment undone in reverse
-// order; v is clamped at zero against rounding).
+// order; v is clamped at zero against rounding).  Undoing the first step
+// restores the zero initial moments exactly: recomputed ones would hold fp32
+// rounding residue, which the next step's m / sqrt(v) would amplify.
 __device__ __forceinline__ float adam_undo(float p, float g, float& m, float& v, bool decay,
                                            float lr, float b1, float b2, float eps, float wd,
-                                           float step_size, float inv_sqrt_bc2, float gs) {
+                                           float step_size, float inv_sqrt_bc2, float gs, bool first) {
   g *= gs;
   p += step_size * m / (sqrtf(v) * inv_sqrt_bc2 + eps);
   if (decay) p /= (1.f - lr * wd);
-  v = fmaxf((v - (1.f - b2) * g * g) / b2, 0.f);
-  m = (m - (1.f - b1) * g) / b1;
+  v = first ? 0.f : fmaxf((v - (1.f - b2) * g * g) / b2, 0.f);
+  m = first ? 0.f : (m - (1.f - b1) * g) / b1;
   return p;
 }
 
@@ -62,14 +64,15 @@ __global__ __launch_bounds__(NT) void adamw_undo_k(float4* __restrict__ p, const
                                                    float4* __restrict__ m, float4* __restrict__ v,
                                                    bf16* __restrict__ wb, long n4, long nd4, float lr,
                                                    float b1, float b2, float eps, float wd,
-                                                   float step_size, float inv_sqrt_bc2, float gs) {
+                                                   float step_size, float inv_sqrt_bc2, float gs,
+                                                   int first) {
   for (long i = blockIdx.x * (long)NT + threadIdx.x; i < n4; i += (long)gridDim.x * NT) {
     float4 pp = p[i], gg = g[i], mm = m[i], vv = v[i];
-    const bool dec = i < nd4;
-    pp.x = adam_undo(pp.x, gg.x, mm.x, vv.x, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
-    pp.y = adam_undo(pp.y, gg.y, mm.y, vv.y, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
-    pp.z = adam_undo(pp.z, gg.z, mm.z, vv.z, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
-    pp.w = adam_undo(pp.w, gg.w, mm.w, vv.w, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
+    const bool dec = i < nd4, f = first != 0;
+    pp.x = adam_undo(pp.x, gg.x, mm.x, vv.x, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs, f);
+    pp.y = adam_undo(pp.y, gg.y, mm.y, vv.y, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs, f);
+    pp.z = adam_undo(pp.z, gg.z, mm.z, vv.z, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs, f);
+    pp.w = adam_undo(pp.w, gg.w, mm.w, vv.w, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs, f);
     p[i] = pp;
     m[i] = mm;
     v[i] = vv;
@@ -145,12 +148,12 @@ hipError_t adamw_step(float* p, const float* g, float* m, float* v, void* wb, lo
 
 hipError_t adamw_undo(float* p, const float* g, float* m, float* v, void* wb, long n, long n_decay,
                       float lr, float beta1, float beta2, float eps, float wd, float step_size,
-                      float inv_sqrt_bc2, float grad_scale, hipStream_t s) {
+                      float inv_sqrt_bc2, float grad_scale, int first_step, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if ((n & 3) || (n_decay & 3)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(adamw_undo_k, dim3(grid_for(n / 4)), dim3(NT), 0, s, (float4*)p, (const float4*)g,
                      (float4*)m, (float4*)v, (bf16*)wb, n / 4, n_decay / 4, lr, beta1, beta2, eps,
-                     wd, step_size, inv_sqrt_bc2, grad_scale);
+                     wd, step_size, inv_sqrt_bc2, grad_scale, first_step);
   return hipGetLastError();
 }
 

@@ -61,10 +61,11 @@ hipError_t adamw_step(float* p, const float* g, float* m, float* v, void* wb, lo
                       float lr, float beta1, float beta2, float eps, float wd, float step_size,
                       float inv_sqrt_bc2, float grad_scale, hipStream_t s);
 
-// Inverse of adamw_step for the same step number and gradient (rollback).
+// Inverse of adamw_step for the same step number and gradient (rollback);
+// first_step != 0 restores the zero initial moments exactly.
 hipError_t adamw_undo(float* p, const float* g, float* m, float* v, void* wb, long n, long n_decay,
                       float lr, float beta1, float beta2, float eps, float wd, float step_size,
-                      float inv_sqrt_bc2, float grad_scale, hipStream_t s);
+                      float inv_sqrt_bc2, float grad_scale, int first_step, hipStream_t s);
 
 // Per-block partials over n fp32 gradients (n % 4 == 0): part[b] = sum of
 // squares of the finite entries of grad_scale * g, bad[b] = non-finite count,

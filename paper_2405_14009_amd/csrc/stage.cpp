@@ -605,7 +605,7 @@ rc_status run_rollback(rc_stage* st) {
                     (float*)(st->state + y.off_m), (float*)(st->state + y.off_v),
                     y.bf ? (void*)(st->state + y.off_wb) : nullptr, y.n_total, y.n_mat, a.lr, a.beta1,
                     a.beta2, a.eps, a.weight_decay, (float)(a.lr / bc1), (float)(1.0 / std::sqrt(bc2)),
-                    st->last_scale, st->stream));
+                    st->last_scale, st->t == 1 ? 1 : 0, st->stream));
   return RC_OK;
 }
 
