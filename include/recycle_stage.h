@@ -175,6 +175,13 @@ rc_status rc_stage_forward(rc_stage* st, rc_mb mb, const void* x, void* y);
  *         RC_ERR_INVALID_ARG, RC_ERR_HIP. */
 rc_status rc_stage_backward_input(rc_stage* st, rc_mb mb, const void* dy, void* dx);
 
+/* Coupled backward (the conventional reverse pass, B_input and B_weight of
+ * mb in one call): dx as rc_stage_backward_input, then mb's gradients as
+ * rc_stage_backward_weight; logs a B and a W record.  For micro-batches whose
+ * weight pass is not deferred (selective decoupling under a stash limit,
+ * section 3.2 "the memory challenge").  Errors: as rc_stage_backward_input. */
+rc_status rc_stage_backward(rc_stage* st, rc_mb mb, const void* dy, void* dx);
+
 /* B_weight: add mb's parameter gradients (X^T dY per linear, column sums for
  * biases, sum(dout * xhat) / sum(dout) for LayerNorm) into the fp32 gradient
  * buffers; the first weight pass of an iteration overwrites them.  Any order
@@ -236,6 +243,33 @@ rc_status rc_stage_optimizer_rollback(rc_stage* st);
 /* Copy up to cap op-log records into buf (may be NULL when cap == 0); *n
  * receives the total number of records. */
 rc_status rc_stage_op_log(rc_stage* st, rc_op_record* buf, int32_t cap, int32_t* n);
+
+/* Stash accounting (the memory change of each op in the schedule MILP,
+ * section 4.2.2: F adds the activations kept for the backward pass, B_input
+ * swaps them for what the deferred B_weight needs, B_weight frees that).
+ * Read as: F +a_f, B_input +(s_w - a_f), B_weight -s_w, coupled backward
+ * -a_f.  Byte counts are the logical sizes of the kept tensors (no alignment
+ * padding), per micro-batch over all layers:
+ *   a_f = L (E (8 T h + 2 T f) + 16 T + attn),  attn = 4 b heads s (fused
+ *         attention's row statistics) or E b heads s^2 (probabilities);
+ *   s_w = L (E (12 T h + 2 T f) + 16 T);   E = element bytes, T = b s. */
+typedef struct rc_stash_account {
+  uint64_t a_f;    /* bytes a micro-batch holds from its F to its B_input */
+  uint64_t s_w;    /* bytes it holds from its B_input to its B_weight */
+  uint64_t live;   /* bytes held by all micro-batches now (between calls) */
+  uint64_t peak;   /* maximum of live since create or the last reset */
+  uint64_t limit;  /* stash limit, 0 = none */
+} rc_stash_account;
+
+/* Fill *out; reset_peak != 0 sets peak = live first.  Works on dry-run handles. */
+rc_status rc_stage_stash_account(rc_stage* st, rc_stash_account* out, int32_t reset_peak);
+
+/* Stash limit M_limit (bytes, 0 = none): a forward pass that would raise
+ * live above it returns RC_ERR_OUT_OF_STASH with no state change.  Backward
+ * calls are never refused; a caller keeps within the limit by running
+ * deferred weight passes, or the coupled backward, when deferring would not
+ * fit.  Errors: RC_ERR_INVALID_ARG (0 < bytes < a_f). */
+rc_status rc_stage_set_stash_limit(rc_stage* st, uint64_t bytes);
 
 /* Number of micro-batches currently holding a stash slot / a forward-only slot. */
 rc_status rc_stage_stash_usage(rc_stage* st, int32_t* stashed, int32_t* inflight);

@@ -11,6 +11,6 @@ from .stage import (  # noqa: F401
     gelu, gelu_prime, layer_backward_fused, layer_backward_input, layer_backward_weight,
     layer_forward, layer_norm, layer_norm_grad_input, merge_heads, softmax_rows, split_heads,
     stage_backward_fused, stage_backward_input, stage_backward_weight, stage_forward, to_heads,
-    OP_F, OP_B, OP_W, OP_STEP, OP_SKIP, OP_ROLLBACK, adamw_rollback,
+    OP_F, OP_B, OP_W, OP_STEP, OP_SKIP, OP_ROLLBACK, adamw_rollback, stash_bytes,
 )
 from .run import run_oplist, OracleRun  # noqa: F401

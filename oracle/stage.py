@@ -327,6 +327,29 @@ OP_F, OP_B, OP_W, OP_STEP, OP_SKIP, OP_ROLLBACK = 0, 1, 2, 3, 4, 5
 MATRIX_IDS = (2, 4, 8, 10)
 
 
+def stash_bytes(cfg, fused_attention: bool):
+    """Bytes one micro-batch holds between its calls (all layers): (a_f, s_w).
+
+    The memory change of each op in the schedule MILP (section 4.2.2), read
+    as F: +a_f, B_input: +(s_w - a_f), B_weight: -s_w (the printed cases do
+    not net to zero per micro-batch; this reading does).  a_f is what the
+    backward passes need from the forward pass: per layer A, LN1 input X, Q, K,
+    V, O, H, C, U, G (8 T h + 2 T f elements), the LayerNorm mean and rstd
+    (4 fp32 per token) and the attention's kept state: the probabilities
+    (b heads s^2 elements) or, with fused attention, the row log-sum-exp
+    (b heads s fp32).  s_w is what the deferred weight pass needs: the
+    operand pairs of the four linears and the two LayerNorms, 12 T h + 2 T f
+    elements, plus the LayerNorm statistics.  E = 2 (bf16) or 4 (fp32)."""
+    E = 2 if cfg.dtype == "bf16" else 4
+    T = cfg.micro_batch * cfg.seq
+    h, f = cfg.hidden, cfg.ffn
+    rows = cfg.micro_batch * cfg.heads * cfg.seq
+    attn = 4 * rows if fused_attention else E * rows * cfg.seq
+    a_f = cfg.layers * (E * (8 * T * h + 2 * T * f) + 16 * T + attn)
+    s_w = cfg.layers * (E * (12 * T * h + 2 * T * f) + 16 * T)
+    return a_f, s_w
+
+
 class StageError(Exception):
     """code is one of 'BAD_STATE', 'OUT_OF_STASH', 'INVALID_ARG'."""
 
@@ -375,6 +398,11 @@ class OracleStage:
         self.log: List[Tuple[int, int, int, int, int, int]] = []
         self.closed = False          # the last call closed an iteration (step / skip / rollback)
         self.last_step_scale = None  # grad_scale of a step that may still be rolled back
+        # stash accounting; the library keeps fused attention's row statistics
+        # instead of probabilities for bf16 stages with head dimension 128
+        fused = cfg.dtype == "bf16" and cfg.hidden // cfg.heads == 128
+        self.a_f, self.s_w = stash_bytes(cfg, fused)
+        self.live = self.peak = self.limit = 0
 
     # -- bookkeeping -------------------------------------------------------
     def _record(self, op, mb):
@@ -394,9 +422,13 @@ class OracleStage:
             raise StageError("BAD_STATE", f"forward of {mb} twice in iteration {self.iter}")
         if self._n_stashed() >= self.max_stashed or self._n_inflight() >= self.max_inflight:
             raise StageError("OUT_OF_STASH", f"no stash slot for {mb}")
+        if self.limit and self.live + self.a_f > self.limit:
+            raise StageError("OUT_OF_STASH", f"forward of {mb} would exceed the stash limit")
         y, caches = stage_forward(np.asarray(x, dtype=F64), self.params, self.shp)
         self.caches[mb] = caches
         self.state[mb] = "F"
+        self.live += self.a_f
+        self.peak = max(self.peak, self.live)
         self._record(OP_F, mb)
         self.closed = False
         self.last_step_scale = None
@@ -409,6 +441,8 @@ class OracleStage:
         dx, stashes = stage_backward_input(np.asarray(dy, dtype=F64), self.caches.pop(mb), self.params)
         self.wstash[mb] = stashes
         self.state[mb] = "B"
+        self.live += self.s_w - self.a_f
+        self.peak = max(self.peak, self.live)
         self._record(OP_B, mb)
         self.closed = False
         self.last_step_scale = None
@@ -428,9 +462,33 @@ class OracleStage:
             for p, g in enumerate(layer):
                 self.grads[l][p] += g
         self.state[mb] = "W"
+        self.live -= self.s_w
         self._record(OP_W, mb)
         self.closed = False
         self.last_step_scale = None
+
+    def backward(self, mb, dy):
+        """Coupled backward: B_input then B_weight of mb (the peak counts the
+        stash between calls, so the pair changes it by -a_f at once)."""
+        mb = (int(mb[0]), int(mb[1]))
+        if self.state.get(mb) != "F":
+            raise StageError("BAD_STATE", f"backward of {mb} in state {self.state.get(mb)}")
+        peak = self.peak
+        dx = self.backward_input(mb, dy)
+        self.backward_weight(mb)
+        self.peak = peak
+        return dx
+
+    def stash_account(self, reset_peak: bool = False):
+        if reset_peak:
+            self.peak = self.live
+        return {"a_f": self.a_f, "s_w": self.s_w, "live": self.live, "peak": self.peak,
+                "limit": self.limit}
+
+    def set_stash_limit(self, nbytes: int):
+        if nbytes and nbytes < self.a_f:
+            raise StageError("INVALID_ARG", "a stash limit below a_f admits no forward")
+        self.limit = int(nbytes)
 
     def optimizer_step(self, grad_scale: float = 1.0):
         pending = [mb for mb, s in self.state.items() if s != "W"]

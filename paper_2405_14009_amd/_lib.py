@@ -20,7 +20,8 @@ RC_NUM_PARAMS = 12
 # Every symbol the header declares, for load checks.
 EXPORTED = (
     "rc_stage_memory_requirements", "rc_stage_create", "rc_stage_destroy", "rc_stage_load_param",
-    "rc_stage_read", "rc_stage_forward", "rc_stage_backward_input", "rc_stage_backward_weight",
+    "rc_stage_read", "rc_stage_forward", "rc_stage_backward_input", "rc_stage_backward",
+    "rc_stage_backward_weight", "rc_stage_stash_account", "rc_stage_set_stash_limit",
     "rc_stage_backward_weight_many", "rc_stage_optimizer_step", "rc_stage_grad_check",
     "rc_stage_optimizer_skip", "rc_stage_optimizer_rollback", "rc_stage_op_log",
     "rc_stage_stash_usage", "rc_stage_set_stream",
@@ -29,6 +30,11 @@ EXPORTED = (
 
 KERNEL_CLASSES = ("gemm_fwd", "gemm_dgrad", "gemm_wgrad", "attn_fwd", "attn_bwd", "layernorm",
                   "reduce", "adamw", "copy")
+
+
+class RcStashAccount(ctypes.Structure):
+    _fields_ = [("a_f", ctypes.c_uint64), ("s_w", ctypes.c_uint64), ("live", ctypes.c_uint64),
+                ("peak", ctypes.c_uint64), ("limit", ctypes.c_uint64)]
 
 
 class RcStageConfig(ctypes.Structure):
@@ -102,6 +108,9 @@ def load() -> ctypes.CDLL:
         "rc_stage_read": [P, I32, I32, I32, P],
         "rc_stage_forward": [P, RcMb, P, P],
         "rc_stage_backward_input": [P, RcMb, P, P],
+        "rc_stage_backward": [P, RcMb, P, P],
+        "rc_stage_stash_account": [P, ctypes.POINTER(RcStashAccount), I32],
+        "rc_stage_set_stash_limit": [P, ctypes.c_uint64],
         "rc_stage_backward_weight": [P, RcMb],
         "rc_stage_backward_weight_many": [P, ctypes.POINTER(RcMb), I32],
         "rc_stage_optimizer_step": [P, F32],

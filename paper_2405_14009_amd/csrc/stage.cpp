@@ -76,6 +76,7 @@ struct Layout {
   FLayer fl;
   size_t wslot_bytes, fslot_bytes, off_fslots, stash_bytes;
   size_t off_S, off_dS, off_dO, off_dv, off_check, off_part, work_bytes;
+  uint64_t acct_af, acct_sw;
 };
 
 rc_status make_layout(const rc_stage_config* c, Layout& y) {
@@ -173,6 +174,17 @@ rc_status make_layout(const rc_stage_config* c, Layout& y) {
   y.off_dO = take(T * h * E);
   y.off_dv = take(y.flash ? rows * 4 : 0);
   y.off_check = take(8 * GRAD_CHECK_BLOCKS);
+  // Logical stash bytes per micro-batch (tensor sizes, no alignment padding):
+  // from F to B_input the forward-written part of the weight-pass slot (X, A,
+  // O, H, C, G and the LayerNorm statistics) plus the forward-only slot (QKV,
+  // U and the attention row statistics or probabilities); from B_input to
+  // B_weight the whole weight-pass slot.
+  {
+    const uint64_t Th = (uint64_t)T * h, Tf = (uint64_t)T * f, st = 16ull * T;
+    const uint64_t attn = y.flash ? 4ull * rows : (uint64_t)E * ss;
+    y.acct_af = (uint64_t)y.L * (E * (8 * Th + 2 * Tf) + st + attn);
+    y.acct_sw = (uint64_t)y.L * (E * (12 * Th + 2 * Tf) + st);
+  }
   y.off_part = take(4 * colsum_part_floats(y.T, (int)std::max(3 * h, f),
                                            std::min(y.wslots, (int)GEMM_MAX_SEG)));
   y.work_bytes = o;
@@ -203,6 +215,9 @@ struct rc_stage {
   // skip, rollback); a step can be rolled back while it is the last call.
   bool closed = false, can_rollback = false;
   float last_scale = 1.f;
+  // Stash accounting: bytes held by micro-batches between calls, its maximum,
+  // and the limit a forward pass must respect (0: none).
+  uint64_t live = 0, peak = 0, limit = 0;
   // per-kernel profile
   struct Rec {
     int kind;
@@ -752,6 +767,9 @@ rc_status rc_stage_forward(rc_stage* st, rc_mb mb, const void* x, void* y) {
   if (st->free_w.empty() || st->free_f.empty())
     return fail(RC_ERR_OUT_OF_STASH, "no free stash slot for micro-batch (" + std::to_string(mb.j) +
                                          "," + std::to_string(mb.k) + ")");
+  if (st->limit && st->live + st->lay.acct_af > st->limit)
+    return fail(RC_ERR_OUT_OF_STASH, "forward of micro-batch (" + std::to_string(mb.j) + "," +
+                                         std::to_string(mb.k) + ") would exceed the stash limit");
   int ws = take_min(st->free_w), fs = take_min(st->free_f);
   if (!st->dry) {
     rc_status r = run_forward(st, ws, fs, x, y);
@@ -762,6 +780,8 @@ rc_status rc_stage_forward(rc_stage* st, rc_mb mb, const void* x, void* y) {
     }
   }
   st->mbs[key] = {1, ws, fs};
+  st->live += st->lay.acct_af;
+  st->peak = std::max(st->peak, st->live);
   record(st, RC_OP_F, mb.j, mb.k);
   st->closed = false;
   st->can_rollback = false;
@@ -782,9 +802,58 @@ rc_status rc_stage_backward_input(rc_stage* st, rc_mb mb, const void* dy, void* 
   st->free_f.push_back(it->second.fs);
   it->second.fs = -1;
   it->second.state = 2;
+  st->live += st->lay.acct_sw - st->lay.acct_af;
+  st->peak = std::max(st->peak, st->live);
   record(st, RC_OP_B, mb.j, mb.k);
   st->closed = false;
   st->can_rollback = false;
+  return RC_OK;
+}
+
+rc_status rc_stage_backward(rc_stage* st, rc_mb mb, const void* dy, void* dx) {
+  if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
+  if (!st->dry && (!dy || !dx || dy == dx)) return fail(RC_ERR_INVALID_ARG, "dy, dx must be distinct device buffers");
+  auto it = st->mbs.find(std::make_pair(mb.j, mb.k));
+  if (it == st->mbs.end() || it->second.state != 1)
+    return fail(RC_ERR_BAD_STATE, "backward of micro-batch (" + std::to_string(mb.j) + "," +
+                                      std::to_string(mb.k) + ") needs a completed forward and no prior B");
+  if (!st->dry) {
+    rc_status r = run_backward_input(st, it->second.ws, it->second.fs, dy, dx);
+    if (r != RC_OK) return r;
+    const int ws = it->second.ws;
+    r = run_backward_weight(st, &ws, 1);
+    if (r != RC_OK) return r;
+  }
+  st->free_f.push_back(it->second.fs);
+  st->free_w.push_back(it->second.ws);
+  it->second.fs = -1;
+  it->second.ws = -1;
+  it->second.state = 3;
+  st->live -= st->lay.acct_af;
+  record(st, RC_OP_B, mb.j, mb.k);
+  record(st, RC_OP_W, mb.j, mb.k);
+  st->grads_fresh = false;
+  st->closed = false;
+  st->can_rollback = false;
+  return RC_OK;
+}
+
+rc_status rc_stage_stash_account(rc_stage* st, rc_stash_account* out, int32_t reset_peak) {
+  if (!st || !out) return fail(RC_ERR_INVALID_ARG, "bad stash_account arguments");
+  if (reset_peak) st->peak = st->live;
+  out->a_f = st->lay.acct_af;
+  out->s_w = st->lay.acct_sw;
+  out->live = st->live;
+  out->peak = st->peak;
+  out->limit = st->limit;
+  return RC_OK;
+}
+
+rc_status rc_stage_set_stash_limit(rc_stage* st, uint64_t bytes) {
+  if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
+  if (bytes && bytes < st->lay.acct_af)
+    return fail(RC_ERR_INVALID_ARG, "a stash limit below one micro-batch's forward share admits no forward");
+  st->limit = bytes;
   return RC_OK;
 }
 
@@ -812,6 +881,7 @@ rc_status rc_stage_backward_weight_many(rc_stage* st, const rc_mb* mbs, int32_t 
   }
   for (int q = 0; q < n; ++q) {
     MbRec& m = st->mbs[keys[q]];
+    st->live -= st->lay.acct_sw;
     st->free_w.push_back(m.ws);
     m.ws = -1;
     m.state = 3;

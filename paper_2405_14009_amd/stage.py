@@ -141,6 +141,26 @@ class Stage:
                                                   self._check_act(dx, "dx")))
         return dx
 
+    def backward(self, mb, dy=None, dx=None):
+        """Coupled backward of micro-batch (j, k): B_input then its B_weight."""
+        if self.dry_run:
+            L.check(self._lib.rc_stage_backward(self._h, _mb(mb), None, None))
+            return None
+        dx = self._new_act() if dx is None else dx
+        L.check(self._lib.rc_stage_backward(self._h, _mb(mb), self._check_act(dy, "dy"),
+                                            self._check_act(dx, "dx")))
+        return dx
+
+    def stash_account(self, reset_peak: bool = False) -> dict:
+        """Stash bytes: a_f, s_w per micro-batch; live, peak, limit."""
+        a = L.RcStashAccount()
+        L.check(self._lib.rc_stage_stash_account(self._h, ctypes.byref(a), int(bool(reset_peak))))
+        return {"a_f": a.a_f, "s_w": a.s_w, "live": a.live, "peak": a.peak, "limit": a.limit}
+
+    def set_stash_limit(self, nbytes: int) -> None:
+        """Stash limit (bytes, 0 = none) that forward passes respect."""
+        L.check(self._lib.rc_stage_set_stash_limit(self._h, ctypes.c_uint64(int(nbytes))))
+
     def backward_weight(self, mb) -> None:
         """B_weight of micro-batch (j, k): accumulate its parameter gradients."""
         L.check(self._lib.rc_stage_backward_weight(self._h, _mb(mb)))

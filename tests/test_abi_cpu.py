@@ -243,6 +243,142 @@ def test_dry_run_skip_and_rollback_rules_match_oracle():
     assert st.op_log() == [tuple(r) for r in o.log]
 
 
+def _fused(cfg):
+    return cfg.dtype == "bf16" and cfg.hidden // cfg.heads == 128
+
+
+@pytest.mark.parametrize("name", list(CONFIGS) + list(TEST_CONFIGS))
+def test_stash_accounting_matches_oracle(name):
+    """a_f / s_w equal the oracle's analytic counts; live and peak after every
+    op of two iterations of the workload's op list equal the oracle's."""
+    lib_or_skip()
+    from paper_2405_14009_amd import Stage
+    cfg = get_config(name)
+    st = Stage.from_config(cfg, dry_run=True)
+    o = oracle.OracleStage(cfg.with_(layers=0), [])
+    o.a_f, o.s_w = oracle.stash_bytes(cfg, _fused(cfg))
+    acct = st.stash_account()
+    assert (acct["a_f"], acct["s_w"]) == (o.a_f, o.s_w)
+    z = np.zeros((1, 1, 1))
+    for op in op_list(cfg) * 2:
+        if op.kind == "F":
+            st.forward(op.mb); o.forward(op.mb, z)
+        elif op.kind == "B":
+            st.backward_input(op.mb); o.backward_input(op.mb, z)
+        elif op.kind == "W":
+            st.backward_weight(op.mb); o.backward_weight(op.mb)
+        else:
+            st.optimizer_step(); o.optimizer_step()
+        a = st.stash_account()
+        assert (a["live"], a["peak"]) == (o.live, o.peak), op
+    assert st.stash_account()["live"] == 0
+
+
+def test_stash_byte_formulas_pinned_by_the_oracles_arrays():
+    """The element terms of a_f and s_w equal the sizes of the arrays the
+    oracle's own decoupled backward keeps (its forward cache and its
+    weight-pass stash), which are chosen by what the passes read, not by the
+    formula: cache = 8 T h + 2 T f + attention probabilities (+ the LN rstd);
+    weight stash = 12 T h + 2 T f."""
+    from oracle import stage as ost
+    cfg = get_config("tiny").with_(layers=2, micro_batch=2, seq=16, hidden=64, heads=2, ffn=128,
+                                   dtype="f32")
+    params = [[p.astype(np.float64) for p in layer] for layer in gen_params(cfg)]
+    from synth import gen_dy, gen_x
+    x = gen_x(cfg, 0).astype(np.float64)
+    shp = ost.LayerShape(cfg.heads, cfg.causal, cfg.ln_eps)
+    y, caches = ost.stage_forward(x, params, shp)
+    dx, stashes = ost.stage_backward_input(gen_dy(cfg, 0).astype(np.float64), caches, params)
+    T, h, f = cfg.micro_batch * cfg.seq, cfg.hidden, cfg.ffn
+    probs = cfg.micro_batch * cfg.heads * cfg.seq * cfg.seq
+    for c, w in zip(caches, stashes):
+        kept = sum(v.size for k, v in c.items() if k not in ("p", "r1", "r2"))
+        assert kept == 8 * T * h + 2 * T * f
+        assert c["p"].size == probs and c["r1"].size + c["r2"].size == 2 * T
+        assert sum(v.size for v in w.values()) == 12 * T * h + 2 * T * f
+    a_f, s_w = oracle.stash_bytes(cfg, False)
+    assert a_f == cfg.layers * (4 * (8 * T * h + 2 * T * f) + 16 * T + 4 * probs)
+    assert s_w == cfg.layers * (4 * (12 * T * h + 2 * T * f) + 16 * T)
+
+
+def test_stash_limit_refusal_matches_oracle():
+    lib_or_skip()
+    import paper_2405_14009_amd as P
+    cfg = get_config("gpt1.3b")
+    st = P.Stage.from_config(cfg, dry_run=True)
+    o = oracle.OracleStage(cfg.with_(layers=0), [])
+    o.a_f, o.s_w = oracle.stash_bytes(cfg, _fused(cfg))
+    with pytest.raises(P.InvalidArgError):
+        st.set_stash_limit(o.a_f - 1)
+    limit = 3 * o.a_f + o.s_w
+    st.set_stash_limit(limit)
+    o.set_stash_limit(limit)
+    z = np.zeros((1, 1, 1))
+    for op in op_list(cfg):
+        if op.kind == "STEP":
+            break
+        got = want = "OK"
+        fn = {"F": (lambda: st.forward(op.mb), lambda: o.forward(op.mb, z)),
+              "B": (lambda: st.backward_input(op.mb), lambda: o.backward_input(op.mb, z)),
+              "W": (lambda: st.backward_weight(op.mb), lambda: o.backward_weight(op.mb))}[op.kind]
+        try:
+            fn[0]()
+        except (P.OutOfStashError, P.BadStateError) as e:
+            got = type(e).__name__
+        try:
+            fn[1]()
+        except oracle.StageError as e:
+            want = {"OUT_OF_STASH": "OutOfStashError", "BAD_STATE": "BadStateError"}[e.code]
+        assert got == want, op
+    assert st.op_log() == [tuple(r) for r in o.log]
+
+
+@pytest.mark.parametrize("name,slots", [("gpt6.7b", 6), ("gpt6.7b", 1), ("gpt1.3b", 1),
+                                        ("gpt13b", 2), ("gpt6.7b", 0)])
+def test_executor_keeps_the_stash_within_the_limit(name, slots):
+    """Selective decoupling: with a stash limit the executor couples or runs
+    weight passes early so the stash never exceeds it; every micro-batch still
+    runs F, B, W exactly once, in dependency order."""
+    lib_or_skip()
+    from paper_2405_14009_amd import RC_OP_B, RC_OP_F, RC_OP_W, Stage
+    from paper_2405_14009_amd.executor import execute
+    cfg = get_config(name)
+    st = Stage.from_config(cfg, dry_run=True)
+    a = st.stash_account()
+    # room for the schedule's warm-up forwards plus `slots` deferred weight stashes
+    limit = (cfg.warmup + 1) * a["a_f"] + slots * a["s_w"] if slots else 0
+    rep = execute(st, op_list(cfg) * 2, stash_limit=limit)
+    if limit:
+        assert rep.peak <= limit
+    else:
+        assert not rep.coupled and not rep.flushed
+    log = st.op_log()
+    for it in (0, 1):
+        seen = {}
+        for r in log:
+            if r[5] != it or r[1] not in (RC_OP_F, RC_OP_B, RC_OP_W):
+                continue
+            seen.setdefault((r[2], r[3]), []).append(r[1])
+        assert all(v == [RC_OP_F, RC_OP_B, RC_OP_W] for v in seen.values()), seen
+        assert len(seen) == cfg.n_mb
+    if slots == 1:
+        assert rep.coupled or rep.flushed
+
+
+def test_executor_reports_an_infeasible_limit():
+    """A limit below the schedule's warm-up activations cannot be met by any
+    choice of coupling: the forward is refused (no state change)."""
+    lib_or_skip()
+    import paper_2405_14009_amd as P
+    from paper_2405_14009_amd.executor import execute
+    cfg = get_config("gpt6.7b")
+    st = P.Stage.from_config(cfg, dry_run=True)
+    a = st.stash_account()
+    with pytest.raises(P.OutOfStashError):
+        execute(st, op_list(cfg), stash_limit=2 * a["a_f"] + a["s_w"])
+    assert st.stash_account()["live"] <= 2 * a["a_f"] + a["s_w"]
+
+
 def test_product_fails_loudly_without_gpu():
     lib_or_skip()
     import torch
