@@ -320,6 +320,60 @@ rc_status rc_stage_synchronize(rc_stage* st);
 /* Message for the last non-OK status on the calling thread ("" if none). */
 const char* rc_last_error(void);
 
+/* ---- Schedule side (host only, no device work) ------------------------- */
+
+/* Failure Normalization (section 4.2.1, Algorithm 1): assign `failures`
+ * failed workers to pipeline stages so that the estimated extra slots are
+ * least; per_stage[i] (length pp) receives the count for stage i, *overhead
+ * the estimate.  Per-stage cost of x failures: max(0, 3 mb x - 3 (dp - x)
+ * (pp - 1)) (the printed min(0, ...) is read as max); ties go to later
+ * stages; at most dp - 1 failures per stage.
+ * Errors: RC_ERR_INVALID_ARG (dp < 2, pp < 1, mb < 1, failures < 0 or above
+ * pp (dp - 1), NULL outputs). */
+rc_status rc_failure_normalization(int32_t dp, int32_t pp, int32_t mb, int32_t failures,
+                                   int32_t* per_stage, int64_t* overhead);
+
+#define RC_SIM_MAX_ITER 16
+
+/* Unit-slot schedule simulator of dp data-parallel pipelines of pp stages,
+ * mb micro-batches each (sections 3.1-3.3).  F, B_input and B_weight take one
+ * slot, a coupled backward two.  Failed workers' micro-batches go round-robin
+ * to the alive peers of their stage.  Each worker runs a ready backward first,
+ * then a ready forward, then (decoupled) a deferred weight pass, oldest first;
+ * ties in (origin pipeline, index) order.  inflight_cap != 0 caps micro-batches
+ * between F and B on stage i at pp - i (textbook 1F1B depth).  Iteration n+1
+ * starts after every worker finished iteration n, or, staggered, per stage
+ * after every worker of that stage did. */
+typedef struct rc_sim_config {
+  int32_t dp, pp, mb;
+  int32_t decoupled;      /* split B into B_input and a deferred B_weight */
+  int32_t staggered;      /* per-stage optimizer step */
+  int32_t iterations;     /* 1 .. RC_SIM_MAX_ITER */
+  int32_t inflight_cap;
+  int32_t n_failed;
+  const int32_t* failed;  /* n_failed pairs (pipeline k, stage i) */
+} rc_sim_config;
+
+typedef struct rc_sim_result {
+  int32_t makespan;                  /* slots until the last op ends */
+  int32_t workers;                   /* alive workers */
+  int32_t busy_max;                  /* most busy slots of any worker */
+  int32_t reserved;
+  int32_t iter_end[RC_SIM_MAX_ITER]; /* slot at which iteration n's last op ends */
+} rc_sim_result;
+
+/* One simulated op: worker (k_s, stage) runs op (RC_OP_F/B/W) of micro-batch
+ * (j, origin k) of iteration `iter` in slots [slot, slot + dur). */
+typedef struct rc_sim_op {
+  int32_t slot, op, iter, stage, j, k, k_s, dur;
+} rc_sim_op;
+
+/* Simulate; up to cap ops are written to ops (NULL when cap == 0) in start
+ * order, *n_ops receives the total.  Errors: RC_ERR_INVALID_ARG (bad sizes, a
+ * stage without an alive worker, a schedule that cannot progress). */
+rc_status rc_schedule_simulate(const rc_sim_config* cfg, rc_sim_result* res, rc_sim_op* ops,
+                               int32_t cap, int32_t* n_ops);
+
 #ifdef __cplusplus
 }
 #endif

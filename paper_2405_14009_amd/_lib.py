@@ -26,6 +26,7 @@ EXPORTED = (
     "rc_stage_optimizer_skip", "rc_stage_optimizer_rollback", "rc_stage_op_log",
     "rc_stage_stash_usage", "rc_stage_set_stream",
     "rc_stage_synchronize", "rc_stage_profile_enable", "rc_stage_profile_read", "rc_last_error",
+    "rc_failure_normalization", "rc_schedule_simulate",
 )
 
 KERNEL_CLASSES = ("gemm_fwd", "gemm_dgrad", "gemm_wgrad", "attn_fwd", "attn_bwd", "layernorm",
@@ -123,6 +124,8 @@ def load() -> ctypes.CDLL:
         "rc_stage_synchronize": [P],
         "rc_stage_profile_enable": [P, I32],
         "rc_stage_profile_read": [P, ctypes.POINTER(RcKernelStat)],
+        "rc_failure_normalization": [I32, I32, I32, I32, ctypes.POINTER(I32), ctypes.POINTER(ctypes.c_int64)],
+        "rc_schedule_simulate": [P, P, P, I32, ctypes.POINTER(I32)],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)

@@ -1042,3 +1042,6 @@ rc_status rc_stage_profile_read(rc_stage* st, rc_kernel_stat* out) {
 const char* rc_last_error(void) { return g_err.c_str(); }
 
 }  // extern "C"
+
+// Shared with the planner's translation unit: set the thread-local message.
+rc_status rc_set_error(rc_status s, const std::string& msg) { return fail(s, msg); }
