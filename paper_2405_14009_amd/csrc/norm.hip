@@ -104,6 +104,22 @@ __global__ __launch_bounds__(NT) void colsum_part_k(ColSegs sg, long ld, long ro
   if (LN) *(float4*)(part_g + (long)blockIdx.y * n + c) = sgm;
 }
 
+// Middle stage of the column sums: block row g sums partial rows
+// [32 g, 32 g + 32) in order (a fixed tree: partials -> groups of 32 -> final).
+constexpr int MID = 32;
+__global__ __launch_bounds__(NT) void colsum_mid_k(const float* __restrict__ part, int nchunk, int n,
+                                                   float* __restrict__ mid) {
+  const int c = 4 * (blockIdx.x * NT + threadIdx.x);
+  if (c >= n) return;
+  const int r0 = blockIdx.y * MID, r1 = min(nchunk, r0 + MID);
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int r = r0; r < r1; ++r) {
+    const float4 v = *(const float4*)(part + (long)r * n + c);
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  *(float4*)(mid + (long)blockIdx.y * n + c) = s;
+}
+
 __global__ __launch_bounds__(NT) void colsum_final_k(const float* __restrict__ part, int nchunk,
                                                      int n, float* __restrict__ out, int accumulate) {
   const int c = 4 * (blockIdx.x * NT + threadIdx.x);
@@ -121,11 +137,243 @@ __global__ __launch_bounds__(NT) void colsum_final_k(const float* __restrict__ p
   *o = s;
 }
 
+// ---------------------------------------------------------------------------
+// One wave per row with the row held in registers as 16-byte chunks (one HBM
+// pass per tensor; MAXC chunks per lane cover rows of up to 64 * MAXC chunks).
+template <class E>
+struct Chunk {
+  static constexpr int N = 16 / sizeof(E);  // elements per 16-byte chunk
+};
+
+__device__ __forceinline__ void unpack(const uint4& u, const bf16*, float (&f)[8]) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(w[i] << 16);
+    f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void unpack(const uint4& u, const float*, float (&f)[4]) {
+  f[0] = __uint_as_float(u.x);
+  f[1] = __uint_as_float(u.y);
+  f[2] = __uint_as_float(u.z);
+  f[3] = __uint_as_float(u.w);
+}
+__device__ __forceinline__ uint4 pack(const float (&f)[8], const bf16*) {
+  bf16 t[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) t[i] = (bf16)f[i];
+  return *(const uint4*)t;
+}
+__device__ __forceinline__ uint4 pack(const float (&f)[4], const float*) {
+  return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                    __float_as_uint(f[3]));
+}
+
+template <class E, int MAXC>
+__global__ __launch_bounds__(NT) void ln_fwd_wave_k(const E* __restrict__ x, const float* __restrict__ g,
+                                                    const float* __restrict__ b, E* __restrict__ y,
+                                                    float* __restrict__ mean, float* __restrict__ rstd,
+                                                    long rows, int h, float eps) {
+  constexpr int EPC = Chunk<E>::N;
+  const long row = blockIdx.x * (long)(NT / 64) + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int lane = threadIdx.x & 63, nc = h / EPC;
+  const E* xr = x + row * h;
+  uint4 v[MAXC];
+  float s = 0.f;
+#pragma unroll
+  for (int q = 0; q < MAXC; ++q) {
+    const int c = lane + 64 * q;
+    if (c < nc) {
+      v[q] = *(const uint4*)(xr + (long)c * EPC);
+      float f[EPC];
+      unpack(v[q], (const E*)nullptr, f);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) s += f[e];
+    }
+  }
+  const float mu = wave_sum(s) / h;
+  float qv = 0.f;
+#pragma unroll
+  for (int q = 0; q < MAXC; ++q) {
+    if (lane + 64 * q < nc) {
+      float f[EPC];
+      unpack(v[q], (const E*)nullptr, f);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) qv += (f[e] - mu) * (f[e] - mu);
+    }
+  }
+  const float rs = 1.0f / sqrtf(wave_sum(qv) / h + eps);
+  E* yr = y + row * h;
+#pragma unroll
+  for (int q = 0; q < MAXC; ++q) {
+    const int c = lane + 64 * q;
+    if (c < nc) {
+      float f[EPC], gg[EPC], bb[EPC];
+      unpack(v[q], (const E*)nullptr, f);
+#pragma unroll
+      for (int e = 0; e < EPC; e += 4) {
+        *(float4*)(gg + e) = *(const float4*)(g + (long)c * EPC + e);
+        *(float4*)(bb + e) = *(const float4*)(b + (long)c * EPC + e);
+      }
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) f[e] = (f[e] - mu) * rs * gg[e] + bb[e];
+      *(uint4*)(yr + (long)c * EPC) = pack(f, (const E*)nullptr);
+    }
+  }
+  if (lane == 0) {
+    mean[row] = mu;
+    rstd[row] = rs;
+  }
+}
+
+template <class E, int MAXC>
+__global__ __launch_bounds__(NT) void ln_bwd_wave_k(const E* __restrict__ dout, const E* __restrict__ x,
+                                                    const float* __restrict__ mean,
+                                                    const float* __restrict__ rstd,
+                                                    const float* __restrict__ g,
+                                                    const E* __restrict__ resid, E* __restrict__ dx,
+                                                    long rows, int h) {
+  constexpr int EPC = Chunk<E>::N;
+  const long row = blockIdx.x * (long)(NT / 64) + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int lane = threadIdx.x & 63, nc = h / EPC;
+  const float mu = mean[row], rs = rstd[row];
+  uint4 dv[MAXC], xv[MAXC];
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int q = 0; q < MAXC; ++q) {
+    const int c = lane + 64 * q;
+    if (c < nc) {
+      dv[q] = *(const uint4*)(dout + row * h + (long)c * EPC);
+      xv[q] = *(const uint4*)(x + row * h + (long)c * EPC);
+      float d[EPC], xx[EPC], gg[EPC];
+      unpack(dv[q], (const E*)nullptr, d);
+      unpack(xv[q], (const E*)nullptr, xx);
+#pragma unroll
+      for (int e = 0; e < EPC; e += 4) *(float4*)(gg + e) = *(const float4*)(g + (long)c * EPC + e);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) {
+        const float dz = d[e] * gg[e];
+        s1 += dz;
+        s2 += dz * (xx[e] - mu) * rs;
+      }
+    }
+  }
+  const float m1 = wave_sum(s1) / h, m2 = wave_sum(s2) / h;
+#pragma unroll
+  for (int q = 0; q < MAXC; ++q) {
+    const int c = lane + 64 * q;
+    if (c < nc) {
+      float d[EPC], xx[EPC], gg[EPC], r[EPC];
+      unpack(dv[q], (const E*)nullptr, d);
+      unpack(xv[q], (const E*)nullptr, xx);
+      unpack(*(const uint4*)(resid + row * h + (long)c * EPC), (const E*)nullptr, r);
+#pragma unroll
+      for (int e = 0; e < EPC; e += 4) *(float4*)(gg + e) = *(const float4*)(g + (long)c * EPC + e);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) {
+        const float xh = (xx[e] - mu) * rs;
+        r[e] += rs * (d[e] * gg[e] - m1 - xh * m2);
+      }
+      *(uint4*)(dx + row * h + (long)c * EPC) = pack(r, (const E*)nullptr);
+    }
+  }
+}
+
+// Column sums with 16-byte loads: thread = one 16-byte column chunk, block
+// row y = (segment, 64-row chunk); rows unrolled by 8 for loads in flight.
+template <class E, bool LN>
+__global__ __launch_bounds__(NT) void colsum_part16_k(ColSegs sg, long ld, long rows, int n, int cps,
+                                                      float* __restrict__ part_b,
+                                                      float* __restrict__ part_g) {
+  constexpr int EPC = Chunk<E>::N;
+  const int c = EPC * (blockIdx.x * NT + threadIdx.x);
+  if (c >= n) return;
+  const int seg = blockIdx.y / cps, ch = blockIdx.y % cps;
+  const E* dout = (const E*)sg.dout[seg];
+  const E* x = (const E*)sg.x[seg];
+  const float* mean = sg.mean[seg];
+  const float* rstd = sg.rstd[seg];
+  const long r0 = (long)ch * CHUNK;
+  const int nr = (int)min((long)CHUNK, rows - r0);
+  float sb[EPC], sgm[EPC];
+#pragma unroll
+  for (int e = 0; e < EPC; ++e) sb[e] = sgm[e] = 0.f;
+  for (int r = 0; r < nr; r += 8) {
+    uint4 dvv[8], xvv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (r + u < nr) {
+        dvv[u] = *(const uint4*)(dout + (r0 + r + u) * ld + c);
+        if (LN) xvv[u] = *(const uint4*)(x + (r0 + r + u) * n + c);
+      }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (r + u < nr) {
+        float d[EPC];
+        unpack(dvv[u], (const E*)nullptr, d);
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) sb[e] += d[e];
+        if (LN) {
+          float xx[EPC];
+          unpack(xvv[u], (const E*)nullptr, xx);
+          const float mu = mean[r0 + r + u], rs = rstd[r0 + r + u];
+#pragma unroll
+          for (int e = 0; e < EPC; ++e) sgm[e] += d[e] * (xx[e] - mu) * rs;
+        }
+      }
+  }
+#pragma unroll
+  for (int e = 0; e < EPC; e += 4) {
+    *(float4*)(part_b + (long)blockIdx.y * n + c + e) = make_float4(sb[e], sb[e + 1], sb[e + 2], sb[e + 3]);
+    if (LN)
+      *(float4*)(part_g + (long)blockIdx.y * n + c + e) =
+          make_float4(sgm[e], sgm[e + 1], sgm[e + 2], sgm[e + 3]);
+  }
+}
+
+template <class E, int MAXC>
+void launch_ln_fwd(const void* x, const float* g, const float* b, void* y, float* mean, float* rstd,
+                   long rows, int h, float eps, hipStream_t s) {
+  hipLaunchKernelGGL((ln_fwd_wave_k<E, MAXC>), dim3((unsigned)((rows + 3) / 4)), dim3(NT), 0, s,
+                     (const E*)x, g, b, (E*)y, mean, rstd, rows, h, eps);
+}
+template <class E, int MAXC>
+void launch_ln_bwd(const void* dout, const void* x, const float* mean, const float* rstd, const float* g,
+                   const void* resid, void* dx, long rows, int h, hipStream_t s) {
+  hipLaunchKernelGGL((ln_bwd_wave_k<E, MAXC>), dim3((unsigned)((rows + 3) / 4)), dim3(NT), 0, s,
+                     (const E*)dout, (const E*)x, mean, rstd, g, (const E*)resid, (E*)dx, rows, h);
+}
+
+// chunks per lane of a row of h elements of type E, or 0 when the wave
+// kernels do not apply (h not a multiple of the chunk, or too long)
+int wave_chunks(int elt, int h) {
+  const int epc = 16 / elt;
+  if (h % epc) return 0;
+  const int per = (h / epc + 63) / 64;
+  return per <= 24 ? per : 0;
+}
+
 }  // namespace
 
 hipError_t ln_forward(int elt, const void* x, const float* g, const float* b, void* y, float* mean,
                       float* rstd, long rows, int h, float eps, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
+  if (const int per = wave_chunks(elt, h)) {
+    if (elt == 2) {
+      if (per <= 4) launch_ln_fwd<bf16, 4>(x, g, b, y, mean, rstd, rows, h, eps, s);
+      else if (per <= 8) launch_ln_fwd<bf16, 8>(x, g, b, y, mean, rstd, rows, h, eps, s);
+      else if (per <= 12) launch_ln_fwd<bf16, 12>(x, g, b, y, mean, rstd, rows, h, eps, s);
+      else launch_ln_fwd<bf16, 24>(x, g, b, y, mean, rstd, rows, h, eps, s);
+    } else {
+      if (per <= 4) launch_ln_fwd<float, 4>(x, g, b, y, mean, rstd, rows, h, eps, s);
+      else if (per <= 8) launch_ln_fwd<float, 8>(x, g, b, y, mean, rstd, rows, h, eps, s);
+      else launch_ln_fwd<float, 24>(x, g, b, y, mean, rstd, rows, h, eps, s);
+    }
+    return hipGetLastError();
+  }
   if (elt == 2)
     hipLaunchKernelGGL(ln_fwd_k<bf16>, dim3(rows), dim3(NT), 0, s, (const bf16*)x, g, b, (bf16*)y,
                        mean, rstd, h, eps);
@@ -139,6 +387,19 @@ hipError_t ln_backward(int elt, const void* dout, const void* x, const float* me
                        const float* rstd, const float* g, const void* resid, void* dx, long rows,
                        int h, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
+  if (const int per = wave_chunks(elt, h)) {
+    if (elt == 2) {
+      if (per <= 4) launch_ln_bwd<bf16, 4>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
+      else if (per <= 8) launch_ln_bwd<bf16, 8>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
+      else if (per <= 12) launch_ln_bwd<bf16, 12>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
+      else launch_ln_bwd<bf16, 24>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
+    } else {
+      if (per <= 4) launch_ln_bwd<float, 4>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
+      else if (per <= 8) launch_ln_bwd<float, 8>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
+      else launch_ln_bwd<float, 24>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
+    }
+    return hipGetLastError();
+  }
   if (elt == 2)
     hipLaunchKernelGGL(ln_bwd_k<bf16>, dim3(rows), dim3(NT), 0, s, (const bf16*)dout, (const bf16*)x,
                        mean, rstd, g, (const bf16*)resid, (bf16*)dx, h);
@@ -149,7 +410,8 @@ hipError_t ln_backward(int elt, const void* dout, const void* x, const float* me
 }
 
 long colsum_part_floats(long rows, int n, int nseg) {
-  return 2 * nseg * ((rows + CHUNK - 1) / CHUNK) * (long)n;
+  const long nchunk = nseg * ((rows + CHUNK - 1) / CHUNK);
+  return 2 * (nchunk + (nchunk + MID - 1) / MID) * (long)n;
 }
 
 hipError_t colsum(int elt, bool ln, const ColSegs& sg, int nseg, long ld, long rows, int n, float* dg,
@@ -161,7 +423,21 @@ hipError_t colsum(int elt, bool ln, const ColSegs& sg, int nseg, long ld, long r
   float* part_b = part;
   float* part_g = part + (long)nchunk * n;
   const int cb = (n / 4 + NT - 1) / NT;
-  if (nchunk > 0) {
+  const int epc = 16 / elt;
+  if (nchunk > 0 && n % epc == 0 && ld % epc == 0) {
+    dim3 grid((n / epc + NT - 1) / NT, nchunk);
+    if (elt == 2) {
+      if (ln)
+        hipLaunchKernelGGL((colsum_part16_k<bf16, true>), grid, dim3(NT), 0, s, sg, ld, rows, n, cps, part_b, part_g);
+      else
+        hipLaunchKernelGGL((colsum_part16_k<bf16, false>), grid, dim3(NT), 0, s, sg, ld, rows, n, cps, part_b, part_g);
+    } else {
+      if (ln)
+        hipLaunchKernelGGL((colsum_part16_k<float, true>), grid, dim3(NT), 0, s, sg, ld, rows, n, cps, part_b, part_g);
+      else
+        hipLaunchKernelGGL((colsum_part16_k<float, false>), grid, dim3(NT), 0, s, sg, ld, rows, n, cps, part_b, part_g);
+    }
+  } else if (nchunk > 0) {
     dim3 grid(cb, nchunk);
     if (elt == 2) {
       if (ln)
@@ -175,8 +451,21 @@ hipError_t colsum(int elt, bool ln, const ColSegs& sg, int nseg, long ld, long r
         hipLaunchKernelGGL((colsum_part_k<float, false>), grid, dim3(NT), 0, s, sg, ld, rows, n, cps, part_b, part_g);
     }
   }
-  hipLaunchKernelGGL(colsum_final_k, dim3(cb), dim3(NT), 0, s, (const float*)part_b, nchunk, n, db, accumulate);
-  if (ln)
-    hipLaunchKernelGGL(colsum_final_k, dim3(cb), dim3(NT), 0, s, (const float*)part_g, nchunk, n, dg, accumulate);
+  // partial rows -> groups of MID (wide grid) -> one row per column
+  const float* fin_b = part_b;
+  const float* fin_g = part_g;
+  int nfin = nchunk;
+  if (nchunk > MID) {
+    const int ng = (nchunk + MID - 1) / MID;
+    float* mid_b = part + 2L * nchunk * n;
+    float* mid_g = mid_b + (long)ng * n;
+    hipLaunchKernelGGL(colsum_mid_k, dim3(cb, ng), dim3(NT), 0, s, (const float*)part_b, nchunk, n, mid_b);
+    if (ln) hipLaunchKernelGGL(colsum_mid_k, dim3(cb, ng), dim3(NT), 0, s, (const float*)part_g, nchunk, n, mid_g);
+    fin_b = mid_b;
+    fin_g = mid_g;
+    nfin = ng;
+  }
+  hipLaunchKernelGGL(colsum_final_k, dim3(cb), dim3(NT), 0, s, fin_b, nfin, n, db, accumulate);
+  if (ln) hipLaunchKernelGGL(colsum_final_k, dim3(cb), dim3(NT), 0, s, fin_g, nfin, n, dg, accumulate);
   return hipGetLastError();
 }
