@@ -137,6 +137,14 @@ __device__ __forceinline__ bf16x8 pack_frag(const f32x16 (&p)[2], int t) {
   return v;
 }
 
+// B fragment of the 16-token step `half` of one score block (32 tokens).
+__device__ __forceinline__ bf16x8 pack_half(const f32x16& p, int half) {
+  bf16x8 v;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = (bf16)p[8 * half + e];
+  return v;
+}
+
 // Global 16-byte fragment of a stationary operand: row `row` (zeros when
 // row >= nrows), columns 16 ks + 8 (l / 32) + 0..7.
 __device__ __forceinline__ void load_stationary(bf16x8 (&f)[HD / 16], const bf16* base, long ld, int row,
@@ -189,7 +197,7 @@ __device__ __forceinline__ void block_of(const AttnArgs& p, int nblk, bool longe
 // key block: S^T = K Q^T (16 MFMAs, Q stationary in registers), online
 // softmax per lane (= per query), O^T += V^T P^T (16 MFMAs).
 template <bool CAUSAL>
-__global__ __launch_bounds__(256) void attn_fwd_k(AttnArgs p) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_k(AttnArgs p) {
   __shared__ __attribute__((aligned(1024))) char lds0[2 * TILE64];
   __shared__ __attribute__((aligned(1024))) char lds1[2 * TILE64];
   const int lane = threadIdx.x & 63;
@@ -382,22 +390,18 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_k(AttnArgs p) {
     const char* ot = st + TILE64;
     const float* lse = (const float*)(st + 2 * TILE64);
     const float* dvv = (const float*)(st + 2 * TILE64 + 1024);
-    f32x16 sc[2], dp[2];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      zero(sc[j]);
-      zero(dp[j]);
-    }
-#pragma unroll
-    for (int ks = 0; ks < HD / 16; ++ks)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        sc[j] = mfma(rd_row(qt, ro, j, ks), kf[ks], sc[j]);
-        dp[j] = mfma(rd_row(ot, ro, j, ks), vf[ks], dp[j]);
-      }
     const bool need_mask = CAUSAL && qs < k0w + 31;
+    // the two 32-query halves of the block in turn (one half's scores live)
+#pragma unroll 1
+    for (int j = 0; j < 2; ++j) {
+      f32x16 sc, dp;
+      zero(sc);
+      zero(dp);
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+      for (int ks = 0; ks < HD / 16; ++ks) {
+        sc = mfma(rd_row(qt, ro, j, ks), kf[ks], sc);
+        dp = mfma(rd_row(ot, ro, j, ks), vf[ks], dp);
+      }
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
         const int ql = 32 * j + 8 * rg + 4 * (lane >> 5);
@@ -407,20 +411,22 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_k(AttnArgs p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * rg + e;
-          float pv = __builtin_amdgcn_exp2f(sc[j][r] * p.sl2 - Lv[e]);
+          float pv = __builtin_amdgcn_exp2f(sc[r] * p.sl2 - Lv[e]);
           if (need_mask && key > qs + ql + e) pv = 0.f;
-          sc[j][r] = pv;
-          dp[j][r] = pv * (dp[j][r] - Dv[e]);
+          sc[r] = pv;
+          dp[r] = pv * (dp[r] - Dv[e]);
         }
       }
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const bf16x8 pf = pack_frag(sc, t);
-      const bf16x8 sf = pack_frag(dp, t);
+      for (int hf = 0; hf < 2; ++hf) {
+        const int t = 2 * j + hf;
+        const bf16x8 pf = pack_half(sc, hf);
+        const bf16x8 sf = pack_half(dp, hf);
 #pragma unroll
-      for (int b = 0; b < HD / 32; ++b) {
-        dv[b] = mfma(rd_tr(ot, to, b, t), pf, dv[b]);
-        dk[b] = mfma(rd_tr(qt, to, b, t), sf, dk[b]);
+        for (int b = 0; b < HD / 32; ++b) {
+          dv[b] = mfma(rd_tr(ot, to, b, t), pf, dv[b]);
+          dk[b] = mfma(rd_tr(qt, to, b, t), sf, dk[b]);
+        }
       }
     }
   };
@@ -449,7 +455,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_k(AttnArgs p) {
 // wave and key block: S^T = K Q^T, dP^T = V dO^T (lane column = query),
 // P, dS as above; dQ^T += K^T dS^T.
 template <bool CAUSAL>
-__global__ __launch_bounds__(256) void attn_bwd_q_k(AttnArgs p) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_q_k(AttnArgs p) {
   __shared__ __attribute__((aligned(1024))) char lds0[2 * TILE64];
   __shared__ __attribute__((aligned(1024))) char lds1[2 * TILE64];
   const int lane = threadIdx.x & 63;
@@ -493,36 +499,34 @@ __global__ __launch_bounds__(256) void attn_bwd_q_k(AttnArgs p) {
     if (CAUSAL && k0 > q0 + 31) return;
     const char* kt = st;
     const char* vt = st + TILE64;
-    f32x16 sc[2], dp[2];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      zero(sc[j]);
-      zero(dp[j]);
-    }
-#pragma unroll
-    for (int ks = 0; ks < HD / 16; ++ks)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        sc[j] = mfma(rd_row(kt, ro, j, ks), qf[ks], sc[j]);
-        dp[j] = mfma(rd_row(vt, ro, j, ks), of[ks], dp[j]);
-      }
     const bool need_mask = (CAUSAL && k0 + 63 > q0) || (k0 + 64 > p.s);
+    // the two 32-key halves of the block in turn (one half's scores live)
+#pragma unroll 1
+    for (int j = 0; j < 2; ++j) {
+      if (CAUSAL && k0 + 32 * j > q0 + 31) break;  // this half is after every query of the wave
+      f32x16 sc, dp;
+      zero(sc);
+      zero(dp);
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+      for (int ks = 0; ks < HD / 16; ++ks) {
+        sc = mfma(rd_row(kt, ro, j, ks), qf[ks], sc);
+        dp = mfma(rd_row(vt, ro, j, ks), of[ks], dp);
+      }
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        float pv = __builtin_amdgcn_exp2f(sc[j][r] * p.sl2 - Lq);
+        float pv = __builtin_amdgcn_exp2f(sc[r] * p.sl2 - Lq);
         if (need_mask) {
           const int key = k0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
           if (key >= p.s || (CAUSAL && key > qq)) pv = 0.f;
         }
-        dp[j][r] = pv * (dp[j][r] - Dq);
+        dp[r] = pv * (dp[r] - Dq);
       }
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const bf16x8 sf = pack_frag(dp, t);
+      for (int hf = 0; hf < 2; ++hf) {
+        const bf16x8 sf = pack_half(dp, hf);
 #pragma unroll
-      for (int b = 0; b < HD / 32; ++b) dq[b] = mfma(rd_tr(kt, to, b, t), sf, dq[b]);
+        for (int b = 0; b < HD / 32; ++b) dq[b] = mfma(rd_tr(kt, to, b, 2 * j + hf), sf, dq[b]);
+      }
     }
   };
 
