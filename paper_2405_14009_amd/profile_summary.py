@@ -45,10 +45,16 @@ def sources_digest() -> str:
 
 
 def kernel_class(name: str) -> str:
-    m = re.search(r"gemm_bf16_kernel<\s*\d+,\s*\d+,\s*\d+,\s*(true|false),\s*(true|false)", name)
+    m = re.search(r"gemm_bf16_kernel<\s*\d+,\s*\d+,\s*\d+,\s*(true|false),\s*(true|false),\s*(\d+)", name)
     if m:
-        return {("true", "false"): "gemm_fwd", ("true", "true"): "gemm_dgrad",
-                ("false", "false"): "gemm_wgrad"}.get(m.groups(), "gemm_other")
+        ak, bk, epi = m.group(1), m.group(2), int(m.group(3))
+        if (ak, bk) == ("false", "false"):
+            return "gemm_wgrad"
+        if epi in (1, 2, 3):          # bias / bias + residual / bias + GeLU: the forward products
+            return "gemm_fwd"
+        if (ak, bk) == ("true", "true") and epi in (0, 4):
+            return "gemm_dgrad"
+        return "gemm_other"
     if "gemm_f32" in name:
         return "gemm_f32"
     if "attn_fwd_k" in name:
