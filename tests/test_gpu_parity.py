@@ -249,6 +249,18 @@ T0 = 64
 
 @pytest.mark.parametrize("name", ["gpt1.3b", "gpt6.7b", "gpt13b", "gpt175b"])
 def test_fullsize_prefix_parity(name):
+    _fullsize(name, batched=False)
+
+
+@pytest.mark.parametrize("name", ["gpt6.7b", "gpt13b"])
+def test_fullsize_batched_weight_pass(name):
+    """The launch configuration the benchmark times: consecutive deferred weight
+    passes of the op list run as one batched call (16 micro-batches, a
+    32768-token segmented reduction, for the 6.7B stage)."""
+    _fullsize(name, batched=True)
+
+
+def _fullsize(name, batched):
     cfg = CONFIGS[name]
     log(f"[fullsize] {name}: L={cfg.layers} h={cfg.hidden} a={cfg.heads} f={cfg.ffn} "
         f"s={cfg.seq} b={cfg.micro_batch} n_mb={cfg.n_mb}, prefix t0={T0}")
@@ -268,7 +280,7 @@ def test_fullsize_prefix_parity(name):
     del g
     # 2) dy zero beyond t0: full op list on the GPU, prefix op list on the oracle
     dy_fn = lambda j, k: gen_dy(cfg, j, k, keep_prefix=T0)
-    g = run_gpu(cfg, ops, params=params, dy_fn=dy_fn)
+    g = run_gpu(cfg, _grouped(ops) if batched else ops, params=params, dy_fn=dy_fn)
     o = oracle.run_oplist(pre, ops, params=params,
                           x_fn=lambda j, k: gen_x(cfg, j, k, seq=T0),
                           dy_fn=lambda j, k: gen_dy(cfg, j, k)[:, :T0])
