@@ -1,30 +1,43 @@
-// bf16 GEMM kernel template on CDNA4 matrix cores: v_mfma_f32_32x32x16_bf16,
-// fp32 accumulate.
+// bf16 GEMM kernels on CDNA4 matrix cores: v_mfma_f32_32x32x16_bf16,
+// fp32 accumulate.  Two kernels share the staging and fragment machinery:
+//   gemm_bf16_kernel     256 x 256 workgroup tiles (and test variants);
+//   gemm_bf16_pp_kernel  256 x 128 tiles with a ping-pong schedule and a
+//                        k-split into two wave groups.
 //
-// Tiles.  A BM x BN workgroup tile runs NW waves in a 2 x NW/2 grid; each
-// wave owns a 128 x (BN / (NW/2)) tile of 32x32 MFMA blocks.  The launcher
-// uses NW = 8: 128 x 64 wave tiles for 256x256 tiles and 128 x 32 for 256x128
-// tiles, two waves per SIMD.  With one wave per SIMD (NW = 4, 128 x 128 wave
-// tiles) every barrier, LDS-read wait and full memory-instruction queue left
-// the matrix core idle; with two, the other wave issues MFMAs meanwhile, which
-// measured faster on every stage shape despite the smaller wave tiles.
+// Tiles.  A BM x BN workgroup tile runs NW = 8 waves in KS k-groups; each
+// k-group is a 2 x (NW / KS / 2) grid of 128 x (BN / (NW / KS / 2)) wave tiles
+// of 32x32 MFMA blocks covering the whole workgroup tile.  With eight waves
+// every SIMD runs two, so while one waits on a barrier or on its LDS reads the
+// other issues MFMAs (one wave per SIMD with 128 x 128 wave tiles left the
+// matrix core idle at every such wait).
 //
-// Staging.  k-tiles of 64 are copied from memory straight into LDS by
+// Staging.  k-tiles of BK are copied from memory straight into LDS by
 // buffer-load-to-LDS instructions (each wave instruction deposits 64 lanes x
 // 16 bytes contiguously; out-of-range offsets deposit zeros, so ragged edges
-// need no branches and no registers hold tile data).  Two LDS stages: the
-// copy of tile t+1 is in flight while tile t is multiplied, one barrier per
-// k-tile.
-//   * k-contiguous operand: LDS tile [rows][64], 16-byte chunks XOR-swizzled
+// need no branches and no registers hold tile data).  NST stages form a ring:
+// the copy of tile t + NST - 1 is issued when tile t starts; a wave waits only
+// for its own copies of the oldest stage (vmcnt of the copies issued after
+// it), then one barrier per k-tile publishes that stage and frees the one
+// multiplied before.
+//   * k-contiguous operand: LDS tile [rows][BK], 16-byte chunks XOR-swizzled
 //     by row; fragments are one ds_read_b128 per lane.
 //   * m/n-contiguous operand (the token reduction of the weight-gradient
-//     GEMMs, the [in, out] weights in the forward): LDS tile [64][rows] in
+//     GEMMs, the [in, out] weights in the forward): LDS tile [BK][rows] in
 //     memory order, chunks XOR-swizzled by k-row; fragments are two
 //     ds_read_b64_tr_b16 per lane, which transpose 4x16 blocks across each
 //     16-lane group so every lane receives 8 k-consecutive values of its
 //     row/column, the same operand layout as the k-contiguous case.
-// Within a k-tile the fragments of the next 16-wide k-step are read while the
-// current step's MFMAs issue.
+//
+// What bounds these kernels on MI355X (counters, and variants with one
+// component switched off): the copies.  Each CU keeps about 64 L2 read
+// requests of 128 bytes in flight, so at the observed 300-450 cycles of
+// average latency it receives 18-27 bytes per clock, while a 256 x 256 x 64
+// k-tile (64 KB) feeds 2048 MFMA cycles per SIMD.  Without the copies the same
+// kernels reach 1.5-1.9 PFLOP/s; without the fragment reads they barely
+// change.  Deeper rings (four or five stages of 32), register staging
+// (buffer_load + ds_write), padded leading dimensions and a one-wave-per-SIMD
+// layout did not help; the ping-pong schedule and a tile order whose 32
+// concurrent tiles per XCD share fewer operand panels did (256 x 128 tiles).
 #pragma once
 
 #include "gemm.h"
@@ -32,12 +45,15 @@
 
 namespace {
 
-constexpr int BK = 64;
-
-// k-contiguous tiles: chunk c (8 elements) of row r lives at chunk c ^ swz_k(r).
-// Depends on r mod 32 only (so every 32-row MFMA block of a wave shares it)
-// and spreads any 8, and any 16, consecutive rows over distinct banks.
-__device__ __forceinline__ int swz_k(int r) { return (r & 7) ^ ((r >> 3) & 3); }
+// k-contiguous tiles: chunk c (8 elements) of row r lives at chunk
+// c ^ swz_k<BK>(r).  Depends on r mod 32 only (so every 32-row MFMA block of
+// a wave shares it) and places the 16 rows that one ds_read_b128 pass serves
+// (16 lanes x 16 bytes) on distinct 16-byte bank groups of a 256-byte window.
+template <int BK>
+__device__ __forceinline__ int swz_k(int r) {
+  if constexpr (BK == 64) return (r & 7) ^ ((r >> 3) & 3);  // 2 rows per window, 8 chunks
+  else return (r >> 2) & 3;                                 // 4 rows per window, 4 chunks
+}
 // m/n-contiguous tiles: chunk c of k-row r lives at chunk c ^ swz_mn(r).
 __device__ __forceinline__ int swz_mn(int r) { return (r & 3) << 2; }
 
@@ -45,22 +61,23 @@ __device__ __forceinline__ int swz_mn(int r) { return (r & 3) << 2; }
 // g = wave + NW q (q < NI) of the operand's 1 KB slices (NW waves).  Every slice of a wave
 // differs from its first by a fixed row (k-contiguous) or k-row
 // (m/n-contiguous) step, so two per-lane values describe all of them.
-template <int ROWS, bool KC, int NI, int NW>
+template <int ROWS, bool KC, int NI, int NW, int BK>
 struct Copier {
   uint32_t base;  // byte offset of this lane's row (k-contiguous) / column (m/n-contiguous) in slice 0
   int kk;         // k offset of this lane's data within the k-tile, slice 0
   int mn;         // this lane's row (k-contiguous) / first column (m/n-contiguous), slice 0
-  static constexpr int RPI = KC ? 8 : 512 / ROWS;  // rows (k-contiguous) or k-rows per slice
+  static constexpr int CPR = KC ? BK / 8 : ROWS / 8;  // 16-byte chunks per LDS row
+  static constexpr int RPI = 64 / CPR;                 // LDS rows (k-rows if m/n-contiguous) per slice
+  static_assert(KC || (NW * RPI) % 4 == 0, "slices of a wave keep k mod 4, hence the swizzle");
   __device__ __forceinline__ void init(int wave, long ld, int mn0, int lane) {
     if (KC) {
-      const int row = 8 * wave + (lane >> 3);
-      kk = 8 * ((lane & 7) ^ swz_k(row));  // the same for every slice: rows differ by 32 q
+      const int row = RPI * wave + lane / CPR;
+      kk = 8 * ((lane % CPR) ^ swz_k<BK>(row));  // the same for every slice: rows differ by 64 q or 128 q
       mn = mn0 + row;
       base = (uint32_t)((long)mn * ld * 2);
     } else {
-      constexpr int CPR = ROWS / 8;  // chunks per k-row
       const int krow = RPI * wave + lane / CPR;
-      const int c = (lane % CPR) ^ swz_mn(krow);  // k-rows of later slices differ by a multiple of 4
+      const int c = (lane % CPR) ^ swz_mn(krow);
       kk = krow;
       mn = mn0 + 8 * c;
       base = (uint32_t)(2 * mn);
@@ -73,8 +90,8 @@ struct Copier {
       uint32_t off;
       if (KC) {
         const int k = k0 + kk;
-        const bool ok = (mn + 8 * NW * q < MN) && (k < K);
-        off = ok ? base + (uint32_t)(8 * NW * q) * (uint32_t)(2 * ld) + 2u * k : kOOB;
+        const bool ok = (mn + RPI * NW * q < MN) && (k < K);
+        off = ok ? base + (uint32_t)(RPI * NW * q) * (uint32_t)(2 * ld) + 2u * k : kOOB;
       } else {
         const int k = k0 + kk + NW * RPI * q;
         off = (mn < MN && k < K) ? base + (uint32_t)k * (uint32_t)(2 * ld) : kOOB;
@@ -85,24 +102,25 @@ struct Copier {
 };
 
 // Per-lane byte offsets of a wave's MFMA fragments in a staged operand tile.
-// k-contiguous: off[ks] for k-step ks (block i of 32 rows adds 4096 i).
-// m/n-contiguous: off[b] for 32-row block b (k-step ks adds 32 ks rows of
+// k-contiguous: off[ks] for k-step ks (block i of 32 rows adds 64 BK i).
+// m/n-contiguous: off[b] for 32-row block b (k-step ks adds 16 ks rows of
 // the tile, the second half-read 4 k-rows).
-template <int ROWS, bool KC, int NBLK>
+template <int ROWS, bool KC, int NBLK, int NKS, int BK>
 struct FragOffsets {
-  static constexpr int N = KC ? 4 : NBLK;
+  static constexpr int N = KC ? NKS : NBLK;
   uint32_t off[N];
-  __device__ __forceinline__ void init(int r0, int lane) {
+  // ks0: the first of the NKS k-steps of the k-tile that this wave multiplies.
+  __device__ __forceinline__ void init(int r0, int lane, int ks0) {
     if constexpr (KC) {
       const int r = r0 + (lane & 31);
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const int c = ks * 2 + (lane >> 5);
-        off[ks] = (uint32_t)(r * 128 + ((c ^ swz_k(r)) << 4));
+      for (int ks = 0; ks < NKS; ++ks) {
+        const int c = (ks0 + ks) * 2 + (lane >> 5);
+        off[ks] = (uint32_t)(r * (2 * BK) + ((c ^ swz_k<BK>(r)) << 4));
       }
     } else {
       const int i = lane & 15;
-      const int k = 8 * (lane >> 5) + (i >> 2);
+      const int k = 16 * ks0 + 8 * (lane >> 5) + (i >> 2);
 #pragma unroll
       for (int b = 0; b < NBLK; ++b) {
         const int mn = r0 + 32 * b + 16 * ((lane >> 4) & 1) + 4 * (i & 3);
@@ -113,11 +131,11 @@ struct FragOffsets {
 };
 
 // Fragment of 32-row block b, k-step ks: 8 k-consecutive values of one row per lane.
-template <int ROWS, bool KC, int NBLK>
-__device__ __forceinline__ bf16x8 frag(const char* tile, const FragOffsets<ROWS, KC, NBLK>& fo, int b,
-                                       int ks) {
+template <int ROWS, bool KC, int NBLK, int NKS, int BK>
+__device__ __forceinline__ bf16x8 frag(const char* tile, const FragOffsets<ROWS, KC, NBLK, NKS, BK>& fo,
+                                       int b, int ks) {
   if constexpr (KC) {
-    return *(const bf16x8*)(tile + fo.off[ks] + 4096 * b);
+    return *(const bf16x8*)(tile + fo.off[ks] + 64 * BK * b);
   } else {
     const char* p0 = tile + fo.off[b] + 16 * ks * (ROWS * 2);
     const char* p1 = p0 + 4 * (ROWS * 2);  // k + 4 keeps k % 4, hence the swizzle
@@ -128,14 +146,14 @@ __device__ __forceinline__ bf16x8 frag(const char* tile, const FragOffsets<ROWS,
   }
 }
 
-// MFMAs of one staged k-tile for a wave tile of 4 x TN blocks of 32x32.  The
-// fragments of k-step ks+1 are read while the MFMAs of k-step ks issue;
-// scheduling groups pin that interleave (one MFMA, then that k-step's share
-// of LDS reads) so the reads stay ahead of their use.
-template <int BM, int BN, bool AK, bool BKC, int TN>
+// MFMAs of one staged k-tile for a wave tile of 4 x TN blocks of 32x32 over
+// NKS k-steps.  The fragments of k-step ks+1 are read while the MFMAs of
+// k-step ks issue; scheduling groups pin that interleave (one MFMA, then that
+// k-step's share of LDS reads) so the reads stay ahead of their use.
+template <int BM, int BN, bool AK, bool BKC, int TN, int NKS, int BK>
 __device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][TN], const char* ta, const char* tb,
-                                         const FragOffsets<BM, AK, 4>& fa,
-                                         const FragOffsets<BN, BKC, TN>& fb) {
+                                         const FragOffsets<BM, AK, 4, NKS, BK>& fa,
+                                         const FragOffsets<BN, BKC, TN, NKS, BK>& fb) {
   constexpr int READS = 4 * (AK ? 1 : 2) + TN * (BKC ? 1 : 2);  // LDS read instructions per k-step
   constexpr int NMFMA = 4 * TN;
   constexpr int PER = (READS + NMFMA - 1) / NMFMA;
@@ -146,9 +164,9 @@ __device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][TN], const char* ta, c
   for (int j = 0; j < TN; ++j) bfr[0][j] = frag(tb, fb, j, 0);
   __builtin_amdgcn_sched_group_barrier(0x100, READS, 0);
 #pragma unroll
-  for (int ks = 0; ks < BK / 16; ++ks) {
+  for (int ks = 0; ks < NKS; ++ks) {
     const int c = ks & 1;
-    if (ks + 1 < BK / 16) {
+    if (ks + 1 < NKS) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) af[c ^ 1][i] = frag(ta, fa, i, ks + 1);
 #pragma unroll
@@ -159,7 +177,7 @@ __device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][TN], const char* ta, c
 #pragma unroll
       for (int j = 0; j < TN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][i], bfr[c][j], acc[i][j], 0, 0, 0);
-    if (ks + 1 < BK / 16) {
+    if (ks + 1 < NKS) {
 #pragma unroll
       for (int q = 0; q < NMFMA; ++q) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -171,20 +189,20 @@ __device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][TN], const char* ta, c
   }
 }
 
-// Epilogue through LDS.  For each 32-row block-row of its tile a wave writes
-// its accumulators (MFMA layout: lane l holds column l % 32, rows
-// 8 (r / 4) + 4 (l / 32) + r % 4) to a row-major fp32 LDS tile (rows padded by
-// 8 floats so the two half-waves hit disjoint banks), then re-reads it row by
-// row so each lane applies the epilogue to 4 consecutive columns with vector
-// global accesses.  `sm` is this wave's private LDS region.
-template <int EPI, int TN>
+// Epilogue through LDS.  For each 32-row block-row i in [I0, I1) of its tile
+// a wave writes its accumulators (MFMA layout: lane l holds column l % 32,
+// rows 8 (r / 4) + 4 (l / 32) + r % 4) to a row-major fp32 LDS tile (rows
+// padded by 8 floats so the two half-waves hit disjoint banks), then re-reads
+// it row by row so each lane applies the epilogue to 4 consecutive columns
+// with vector global accesses.  `sm` is this wave's private LDS region.
+template <int EPI, int TN, int I0, int I1>
 __device__ __forceinline__ void epilogue(const GemmParams& p, f32x16 (&acc)[4][TN], float* sm, int m0,
                                          int n0, int lane, long c_off) {
   constexpr int COLS = 32 * TN, STRIDE = COLS + 8;
   typedef typename EpiOut<EPI, bf16>::type OutT;
   void* C = (OutT*)p.C + c_off;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = I0; i < I1; ++i) {
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -203,24 +221,66 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, f32x16 (&acc)[4][T
   }
 }
 
-template <int BM, int BN, int NW, bool AK, bool BKC, int EPI>
+// Reduction of a k-split workgroup: the two k-groups hold partial sums of the
+// same output tile.  Wave (g, w) hands the partial of the block-rows that the
+// other group finishes (rows 2 (1 - g), +1) to its partner through LDS slot
+// `mine`, then adds the partner's partial of its own rows (2 g, +1) from slot
+// `theirs`.  Slots hold [row-block][n-block][register][lane] floats, so every
+// access is 256 contiguous bytes per wave instruction.
+template <int TN, int G>
+__device__ __forceinline__ void ksplit_reduce(f32x16 (&acc)[4][TN], float* mine, const float* theirs,
+                                              int lane) {
+#pragma unroll
+  for (int il = 0; il < 2; ++il)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mine[((il * TN + j) * 16 + r) * 64 + lane] = acc[2 * (1 - G) + il][j][r];
+  __syncthreads();
+#pragma unroll
+  for (int il = 0; il < 2; ++il)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[2 * G + il][j][r] += theirs[((il * TN + j) * 16 + r) * 64 + lane];
+}
+
+// s_waitcnt vmcnt(N), other counters untouched (gfx9 encoding: vmcnt bits
+// [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
+
+template <int BM, int BN, int NW, int KS, int BK, int NST, bool AK, bool BKC, int EPI>
 __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
-  static_assert(BM == 256 && (BN == 256 || BN == 128) && (NW == 4 || NW == 8), "tile shapes");
-  constexpr int WN_ = NW / 2;            // waves along n (2 along m)
+  static_assert(BM == 256 && (BN == 256 || BN == 128) && NW == 8 && (KS == 1 || KS == 2) &&
+                    (BK == 32 || BK == 64) && NST >= 2, "tile shapes");
+  constexpr int NWS = NW / KS;           // waves per k-group
+  constexpr int WN_ = NWS / 2;           // waves along n (2 along m)
   constexpr int TN = BN / (32 * WN_);    // 32-wide blocks per wave along n
+  constexpr int NKS = (BK / 16) / KS;    // k-steps per wave per k-tile
+  static_assert(NKS >= 1, "k-steps");
   constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
   constexpr int STAGE = A_BYTES + B_BYTES;
   constexpr int NA = A_BYTES / 1024, NB = B_BYTES / 1024;  // wave instructions per k-tile
   static_assert(NA % NW == 0 && NB % NW == 0, "copy split");
   constexpr int NIA = NA / NW, NIB = NB / NW;
-  // Two stages as distinct LDS objects, so the compiler can tell that the
-  // copy into one stage does not alias the fragment reads from the other.
-  __shared__ __attribute__((aligned(1024))) char lds0[STAGE];
-  __shared__ __attribute__((aligned(1024))) char lds1[STAGE];
+  constexpr int PER_TILE = NIA + NIB;    // copy instructions per wave per k-tile
+  constexpr int EPI_BYTES = 32 * (32 * TN + 8) * 4;  // one wave's epilogue block-row tile
+  // k-split reduction slots: one per wave, 2 block-rows x TN blocks x 4 KB.
+  constexpr int SLOT = 2 * TN * 4096;
+  constexpr int RED_BYTES = KS == 2 ? NW * SLOT : NW * EPI_BYTES;
+  constexpr int LDS_BYTES = NST * STAGE > RED_BYTES ? NST * STAGE : RED_BYTES;
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+  static_assert(EPI_BYTES <= SLOT, "epilogue tile fits a reduction slot");
+  __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm = wave / WN_, wn = wave % WN_;
+  const int kg = wave / NWS, ws = wave % NWS;
+  const int wm = ws / WN_, wn = ws % WN_;
 
   // Tile order: spread consecutive tiles over the 8 XCDs' own ranges, then
   // group tile-rows so concurrently running tiles share operand panels in L2.
@@ -250,14 +310,14 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
   else if (p.krange == KR_ABOVE) kb = (m0 / BK) * BK;
   const int nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
 
-  Copier<BM, AK, NIA, NW> ca;
-  Copier<BN, BKC, NIB, NW> cb;
+  Copier<BM, AK, NIA, NW, BK> ca;
+  Copier<BN, BKC, NIB, NW, BK> cb;
   ca.init(wave, p.lda, m0, lane);
   cb.init(wave, p.ldb, n0, lane);
-  FragOffsets<BM, AK, 4> fa;
-  FragOffsets<BN, BKC, TN> fb;
-  fa.init(wm * 128, lane);
-  fb.init(wn * (BN / WN_), lane);
+  FragOffsets<BM, AK, 4, NKS, BK> fa;
+  FragOffsets<BN, BKC, TN, NKS, BK> fb;
+  fa.init(wm * 128, lane, kg * NKS);
+  fb.init(wn * (BN / WN_), lane, kg * NKS);
 
   f32x16 acc[4][TN];
 #pragma unroll
@@ -267,9 +327,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // Tile t lives in stage t % 2.  The copy of tile t+1 is issued before the
-  // MFMAs of tile t.  With a segmented reduction the k-tile's segment selects
-  // the operand bases (a k-tile never straddles segments).
+  // With a segmented reduction the k-tile's segment selects the operand bases
+  // (a k-tile never straddles segments).
   auto issue = [&](char* st, int k0) {
     if (p.kseg_len > 0) {
       const int sg = k0 / p.kseg_len, kin = k0 - sg * p.kseg_len;
@@ -284,25 +343,262 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
       cb.issue(rb, st + A_BYTES, wave, p.ldb, p.N, k0, ke);
     }
   };
-  if (nk > 0) issue(lds0, kb);
-  stage_sync();
-  int t = 0;
-  for (; t + 1 < nk; t += 2) {
-    issue(lds1, kb + (t + 1) * BK);
-    mma_tile<BM, BN, AK, BKC, TN>(acc, lds0, lds0 + A_BYTES, fa, fb);
-    stage_sync();
-    if (t + 2 < nk) issue(lds0, kb + (t + 2) * BK);
-    mma_tile<BM, BN, AK, BKC, TN>(acc, lds1, lds1 + A_BYTES, fa, fb);
-    stage_sync();
+  // Ring of NST stages: tile t lives in stage t mod NST.  Tiles 0 .. NST-2 are
+  // issued up front; iteration t waits for tile t, publishes it with the
+  // barrier (which also certifies that every wave is done with tile t-1), then
+  // refills tile t-1's stage with tile t + NST - 1 and multiplies tile t.
+#pragma unroll
+  for (int i = 0; i < NST - 1; ++i)
+    if (i < nk) issue(lds + i * STAGE, kb + i * BK);
+  int sc = 0, si = NST - 1;  // stage of tile t, stage that tile t + NST - 1 goes to
+  for (int t = 0; t < nk; ++t) {
+    __builtin_amdgcn_sched_barrier(0);
+    if (t + NST - 2 < nk) wait_vmcnt<(NST - 2) * PER_TILE>();  // tiles t+1 .. t+NST-2 may stay in flight
+    else wait_vmcnt<0>();
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    if (t + NST - 1 < nk) issue(lds + si * STAGE, kb + (t + NST - 1) * BK);
+    const char* st = lds + sc * STAGE;
+    mma_tile<BM, BN, AK, BKC, TN, NKS, BK>(acc, st, st + A_BYTES, fa, fb);
+    sc = sc + 1 == NST ? 0 : sc + 1;
+    si = si + 1 == NST ? 0 : si + 1;
   }
-  if (t < nk) mma_tile<BM, BN, AK, BKC, TN>(acc, lds0, lds0 + A_BYTES, fa, fb);
+
+  // LDS is free once every wave is past its last k-tile.
+  __builtin_amdgcn_sched_barrier(0);
+  __syncthreads();
+  if constexpr (KS == 2) {
+    float* mine = (float*)(lds + wave * SLOT);
+    float* theirs = (float*)(lds + ((1 - kg) * NWS + ws) * SLOT);
+    // The partner's slot is read only by this wave, so after the reduction it
+    // serves as this wave's epilogue tile.
+    if (kg == 0) {
+      ksplit_reduce<TN, 0>(acc, mine, theirs, lane);
+      epilogue<EPI, TN, 0, 2>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
+    } else {
+      ksplit_reduce<TN, 1>(acc, mine, theirs, lane);
+      epilogue<EPI, TN, 2, 4>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
+    }
+  } else {
+    float* sm = (float*)(lds + wave * EPI_BYTES);
+    epilogue<EPI, TN, 0, 4>(p, acc, sm, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
+  }
+}
+
+// Fragments of one unit (two consecutive k-steps, 2 u and 2 u + 1 of the
+// wave's NKS) of a staged k-tile.
+template <int BM, int BN, bool AK, bool BKC, int TN, int NKS, int BK>
+__device__ __forceinline__ void load_unit(bf16x8 (&af)[2][4], bf16x8 (&bfr)[2][TN], const char* ta,
+                                          const char* tb, const FragOffsets<BM, AK, 4, NKS, BK>& fa,
+                                          const FragOffsets<BN, BKC, TN, NKS, BK>& fb, int u) {
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) af[s][i] = frag(ta, fa, i, 2 * u + s);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bfr[s][j] = frag(tb, fb, j, 2 * u + s);
+  }
+}
+
+template <int TN>
+__device__ __forceinline__ void mma_unit(f32x16 (&acc)[4][TN], const bf16x8 (&af)[2][4],
+                                         const bf16x8 (&bfr)[2][TN]) {
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s][i], bfr[s][j], acc[i][j], 0, 0, 0);
+}
+
+// Workgroup-wide barrier that the compiler may not move any instruction across.
+__device__ __forceinline__ void phase_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Ping-pong schedule.  Waves w and w + 4 share a SIMD (waves are dealt to the
+// four SIMDs in turn); the two groups {0..3} and {4..7} run the same
+// sequence of alternating phases, one phase apart:
+//   memory phase:  issue this wave's share of a k-tile copy (first unit of a
+//                  tile only), read one unit's fragments (two k-steps) from
+//                  LDS into registers and wait for them;
+//   compute phase: the unit's 4 x TN x 2 MFMAs from registers, no LDS access.
+// Every phase ends at a workgroup barrier, so while one group multiplies the
+// other reads, and each SIMD always has one wave with MFMAs to issue: the
+// matrix core no longer idles while both waves of a SIMD sit at the same
+// barrier or wait on LDS at the same time.
+//   KS = 1 (256 x 256 tiles): group g owns rows 128 g .. 128 g + 127 (four
+//   128 x 64 wave tiles), two units per k-tile.
+//   KS = 2 (256 x 128 tiles): each group covers the whole tile with four
+//   128 x 64 wave tiles and multiplies k-steps 2 g, 2 g + 1 of every k-tile
+//   (one unit); the partial sums are added through LDS at the end.
+// Copies.  Tile t + NST - 1 is issued in the memory phase of tile t's first
+// unit.  Tile t + 1 is first read in group 0's first memory phase of tile
+// t + 1; before the barrier that opens that phase each wave waits for its own
+// share (group 0 after its last compute phase of tile t, group 1 after its
+// last memory phase of tile t).  The stage being refilled held tile t - 1,
+// whose last fragment reads (group 1's last memory phase of tile t - 1)
+// completed before the barrier that opens group 0's first phase of tile t.
+template <int BN, int KS, int NST, int GM, bool AK, bool BKC, int EPI>
+__global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
+  constexpr int BM = 256, NW = 8, BK = 64;
+  static_assert((BN == 256 && KS == 1) || (BN == 128 && KS == 2), "tile shapes");
+  static_assert(NST >= 2 && (KS == 1 || NST >= 3), "a k-split group must issue a copy two phases ahead");
+  constexpr int NWS = NW / KS;           // waves per k-group
+  constexpr int WN_ = NWS / 2;           // waves along n (2 along m)
+  constexpr int TN = BN / (32 * WN_);    // 32-wide blocks per wave along n (2)
+  constexpr int NKS = (BK / 16) / KS;    // k-steps per wave per k-tile
+  constexpr int U = NKS / 2;             // units per wave per k-tile
+  constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
+  constexpr int STAGE = A_BYTES + B_BYTES;
+  constexpr int NA = A_BYTES / 1024, NB = B_BYTES / 1024;
+  static_assert(NA % NW == 0 && NB % NW == 0, "copy split");
+  constexpr int NIA = NA / NW, NIB = NB / NW;
+  constexpr int PER_TILE = NIA + NIB;
+  constexpr int EPI_BYTES = 32 * (32 * TN + 8) * 4;
+  constexpr int SLOT = 2 * TN * 4096;
+  constexpr int RED_BYTES = KS == 2 ? NW * SLOT : NW * EPI_BYTES;
+  constexpr int LDS_BYTES = NST * STAGE > RED_BYTES ? NST * STAGE : RED_BYTES;
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+  __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int grp = wave >> 2;             // ping-pong group
+  const int kg = wave / NWS, ws = wave % NWS;
+  const int wm = ws / WN_, wn = ws % WN_;
+
+  const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
+  int pid = blockIdx.x;
+  const int ntiles = gridDim.x;
+  if ((ntiles & 7) == 0) pid = (pid & 7) * (ntiles >> 3) + (pid >> 3);
+  const int width = GM * tiles_n;
+  const int first_m = (pid / width) * GM;
+  const int gsz = min(tiles_m - first_m, GM);
+  const int tm = first_m + (pid % width) % gsz;
+  const int tn = (pid % width) / gsz;
+  const int m0 = tm * BM, n0 = tn * BN;
+  if (p.causal_skip && n0 > m0 + BM - 1) return;
+
+  const int z = blockIdx.y;
+  const int zb = z / p.heads, zh = z % p.heads;
+  const bf16* A = (const bf16*)p.A + zb * p.a_bs + zh * p.a_hs;
+  const bf16* B = (const bf16*)p.B + zb * p.b_bs + zh * p.b_hs;
+  const long c_off = zb * p.c_bs + zh * p.c_hs;
+  const i32x4 ra = make_rsrc(A, 2L * (AK ? (long)p.M * p.lda : (long)p.K * p.lda));
+  const i32x4 rb = make_rsrc(B, 2L * (BKC ? (long)p.N * p.ldb : (long)p.K * p.ldb));
+
+  int kb = 0, ke = p.K;
+  if (p.krange == KR_BELOW) ke = min(p.K, m0 + BM);
+  else if (p.krange == KR_ABOVE) kb = (m0 / BK) * BK;
+  const int nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
+
+  Copier<BM, AK, NIA, NW, BK> ca;
+  Copier<BN, BKC, NIB, NW, BK> cb;
+  ca.init(wave, p.lda, m0, lane);
+  cb.init(wave, p.ldb, n0, lane);
+  FragOffsets<BM, AK, 4, NKS, BK> fa;
+  FragOffsets<BN, BKC, TN, NKS, BK> fb;
+  fa.init(wm * 128, lane, kg * NKS);
+  fb.init(wn * (BN / WN_), lane, kg * NKS);
+
+  f32x16 acc[4][TN];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  auto issue = [&](char* st, int k0) {
+    if (p.kseg_len > 0) {
+      const int sg = k0 / p.kseg_len, kin = k0 - sg * p.kseg_len;
+      const i32x4 sa = make_rsrc((const bf16*)p.segA[sg] + zb * p.a_bs + zh * p.a_hs,
+                                 2L * (AK ? (long)p.M * p.lda : (long)p.kseg_len * p.lda));
+      const i32x4 sb = make_rsrc((const bf16*)p.segB[sg] + zb * p.b_bs + zh * p.b_hs,
+                                 2L * (BKC ? (long)p.N * p.ldb : (long)p.kseg_len * p.ldb));
+      ca.issue(sa, st, wave, p.lda, p.M, kin, p.kseg_len);
+      cb.issue(sb, st + A_BYTES, wave, p.ldb, p.N, kin, p.kseg_len);
+    } else {
+      ca.issue(ra, st, wave, p.lda, p.M, k0, ke);
+      cb.issue(rb, st + A_BYTES, wave, p.ldb, p.N, k0, ke);
+    }
+  };
+  // Waits until this wave's share of tile t + 1 has landed (the copies of
+  // tiles t + 2 .. t + NST - 1 may stay in flight).
+  auto wait_next = [&](int t) {
+    if (t + NST - 1 < nk) wait_vmcnt<(NST - 2) * PER_TILE>();
+    else wait_vmcnt<0>();
+  };
+
+  // Prologue: tiles 0 .. NST-2 land before either group starts.
+#pragma unroll
+  for (int i = 0; i < NST - 1; ++i)
+    if (i < nk) issue(lds + i * STAGE, kb + i * BK);
+  wait_vmcnt<0>();
+  __syncthreads();
+  if (grp == 1) phase_barrier();
+
+  bf16x8 af[2][4], bfr[2][TN];
+  int sc = 0, si = NST - 1;  // stage of tile t, stage that tile t + NST - 1 goes to
+  for (int t = 0; t < nk; ++t) {
+    const char* st = lds + sc * STAGE;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      // memory phase
+      if (u == 0 && t + NST - 1 < nk) issue(lds + si * STAGE, kb + (t + NST - 1) * BK);
+      load_unit<BM, BN, AK, BKC, TN, NKS, BK>(af, bfr, st, st + A_BYTES, fa, fb, u);
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the unit's fragments are in registers
+      if (grp == 1 && u == U - 1) wait_next(t);
+      phase_barrier();
+      // compute phase
+      mma_unit<TN>(acc, af, bfr);
+      if (grp == 0 && u == U - 1) wait_next(t);
+      phase_barrier();
+    }
+    sc = sc + 1 == NST ? 0 : sc + 1;
+    si = si + 1 == NST ? 0 : si + 1;
+  }
+  if (grp == 0) phase_barrier();
 
   // LDS is free once every wave is past its last k-tile.
   __syncthreads();
-  constexpr int EPI_BYTES = 32 * (32 * TN + 8) * 4;  // one wave's block-row tile
-  static_assert((NW / 2) * EPI_BYTES <= STAGE, "epilogue tiles fit NW/2 per stage");
-  float* sm = (float*)((wave < NW / 2 ? lds0 : lds1) + (wave % (NW / 2)) * EPI_BYTES);
-  epilogue<EPI, TN>(p, acc, sm, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
+  if constexpr (KS == 2) {
+    float* mine = (float*)(lds + wave * SLOT);
+    float* theirs = (float*)(lds + ((1 - kg) * NWS + ws) * SLOT);
+    if (kg == 0) {
+      ksplit_reduce<TN, 0>(acc, mine, theirs, lane);
+      epilogue<EPI, TN, 0, 2>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
+    } else {
+      ksplit_reduce<TN, 1>(acc, mine, theirs, lane);
+      epilogue<EPI, TN, 2, 4>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
+    }
+  } else {
+    float* sm = (float*)(lds + wave * EPI_BYTES);
+    epilogue<EPI, TN, 0, 4>(p, acc, sm, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
+  }
+}
+
+template <int BN, int KS, int NST, int GM, bool AK, bool BKC, int EPI>
+hipError_t launch_bf16_pp(const GemmParams& p, hipStream_t s) {
+  const long z = (long)p.batch * p.heads;
+  const int tiles = ((p.M + 255) / 256) * ((p.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_bf16_pp_kernel<BN, KS, NST, GM, AK, BKC, EPI>), dim3(tiles, z), dim3(512), 0, s,
+                     p);
+  return hipGetLastError();
+}
+
+// Launch of one kernel variant over the whole (tiles, batch x heads) grid.
+template <int BM, int BN, int NW, int KS, int BK, int NST, bool AK, bool BKC, int EPI>
+hipError_t launch_bf16_variant(const GemmParams& p, hipStream_t s) {
+  const long z = (long)p.batch * p.heads;
+  const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, NW, KS, BK, NST, AK, BKC, EPI>), dim3(tiles, z),
+                     dim3(64 * NW), 0, s, p);
+  return hipGetLastError();
 }
 
 template <bool AK, bool BKC, int EPI>
@@ -315,16 +611,12 @@ hipError_t launch_bf16(const GemmParams& p, hipStream_t s) {
   // Tile choice: the fewest (waves of 256 workgroups) x (tile area), i.e. the
   // least padded work on 256 compute units; ties go to the larger tile, which
   // re-reads its operands less.
-  // 8 waves (2 per SIMD): while one wave of a SIMD waits on a barrier or
-  // its LDS reads, the other issues MFMAs.
-  if (p.N <= 128 || cost(256, 128) < cost(256, 256)) {
-    const int tiles = ((p.M + 255) / 256) * ((p.N + 127) / 128);
-    hipLaunchKernelGGL((gemm_bf16_kernel<256, 128, 8, AK, BKC, EPI>), dim3(tiles, z), dim3(512), 0, s, p);
-  } else {
-    const int tiles = ((p.M + 255) / 256) * ((p.N + 255) / 256);
-    hipLaunchKernelGGL((gemm_bf16_kernel<256, 256, 8, AK, BKC, EPI>), dim3(tiles, z), dim3(512), 0, s, p);
-  }
-  return hipGetLastError();
+  // 256 x 128 tiles run the ping-pong k-split kernel (three stages, tile-rows
+  // grouped by four); 256 x 256 tiles the plain two-stage kernel, which
+  // measured as fast as its ping-pong form.
+  if (p.N <= 128 || cost(256, 128) < cost(256, 256))
+    return launch_bf16_pp<128, 2, 3, 4, AK, BKC, EPI>(p, s);
+  return launch_bf16_variant<256, 256, 8, 1, 64, 2, AK, BKC, EPI>(p, s);
 }
 
 }  // namespace
