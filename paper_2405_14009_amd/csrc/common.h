@@ -16,10 +16,11 @@ template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf
 // tanh form of GeLU: 0.5 u (1 + tanh(z)), z = sqrt(2/pi) (u + 0.044715 u^3).
 // Evaluated through the identity 0.5 (1 + tanh z) = 1 / (1 + exp(-2 z)),
 // which needs one exponential and one reciprocal and has no cancellation.
+// The reciprocal is the hardware one (1 ulp; 1 / inf = 0 for large -u).
 __device__ __forceinline__ float gelu_sig(float u) {
   const float c = 0.7978845608028654f;
   const float z = c * (u + 0.044715f * u * u * u);
-  return 1.0f / (1.0f + __expf(-2.0f * z));
+  return __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * z));
 }
 
 __device__ __forceinline__ float gelu_f(float u) { return u * gelu_sig(u); }

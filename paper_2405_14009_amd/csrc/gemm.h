@@ -88,18 +88,56 @@ __device__ __forceinline__ void epi_store(const GemmParams& p, E* C, int m, int 
   }
 }
 
-// Same epilogue on 4 consecutive columns n..n+3 (n % 4 == 0, all in range);
-// 8- or 16-byte vector accesses.
+// Per-element input of an epilogue at (m, n..n+3): the residual, GeLU's
+// input, or the fp32 gradient being accumulated into.  Fetched separately
+// from the arithmetic so that a tile's epilogue can have a whole block-row of
+// these loads in flight instead of one load round trip per output group.
+template <int EPI>
+struct EpiIn {
+  static constexpr bool kHas = EPI == EPI_BIAS_RESID || EPI == EPI_GELU_BWD || EPI == EPI_F32_ACC;
+  uint4 raw;
+};
+
 template <int EPI, class E>
-__device__ __forceinline__ void epi_store4(const GemmParams& p, void* Cv, int m, int n, float4 v) {
-  const long i = (long)m * p.ldc + n;
-  auto ld4 = [](const E* q) -> float4 {
+__device__ __forceinline__ EpiIn<EPI> epi_fetch4(const GemmParams& p, const void* Cv, int m, int n) {
+  EpiIn<EPI> r;
+  r.raw = make_uint4(0, 0, 0, 0);
+  auto ld = [](const E* q) -> uint4 {
     if constexpr (sizeof(E) == 2) {
       const uint2 u = *(const uint2*)q;
+      return make_uint4(u.x, u.y, 0, 0);
+    } else {
+      return *(const uint4*)q;
+    }
+  };
+  if constexpr (EPI == EPI_BIAS_RESID) {
+    r.raw = ld((const E*)p.resid + (long)m * p.ld_resid + n);
+  } else if constexpr (EPI == EPI_GELU_BWD) {
+    r.raw = ld((const E*)p.aux + (long)m * p.ld_aux + n);
+  } else if constexpr (EPI == EPI_F32_ACC) {
+    if (p.accumulate) r.raw = *(const uint4*)((const float*)Cv + (long)m * p.ldc + n);
+  }
+  return r;
+}
+
+constexpr bool epi_has_bias(int epi) {
+  return epi == EPI_BIAS || epi == EPI_BIAS_RESID || epi == EPI_BIAS_GELU;
+}
+
+// The epilogue on 4 consecutive columns n..n+3 (n % 4 == 0, all in range)
+// given their fetched input and bias[n..n+3] (loaded once by the caller: a
+// lane's columns are the same on every row); 8- or 16-byte vector stores.
+template <int EPI, class E>
+__device__ __forceinline__ void epi_finish4(const GemmParams& p, void* Cv, int m, int n, float4 v,
+                                            const EpiIn<EPI>& in, float4 b) {
+  const long i = (long)m * p.ldc + n;
+  auto cvt4 = [](uint4 u) -> float4 {
+    if constexpr (sizeof(E) == 2) {
       return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
                          __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
     } else {
-      return *(const float4*)q;
+      return make_float4(__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z),
+                         __uint_as_float(u.w));
     }
   };
   auto st4 = [](E* q, float4 f) {
@@ -111,26 +149,24 @@ __device__ __forceinline__ void epi_store4(const GemmParams& p, void* Cv, int m,
     }
   };
   if constexpr (EPI == EPI_F32_ACC) {
-    float4* c = (float4*)((float*)Cv + i);
     if (p.accumulate) {
-      const float4 o = *c;
-      v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+      v.x += __uint_as_float(in.raw.x); v.y += __uint_as_float(in.raw.y);
+      v.z += __uint_as_float(in.raw.z); v.w += __uint_as_float(in.raw.w);
     }
-    *c = v;
+    *(float4*)((float*)Cv + i) = v;
   } else if constexpr (EPI == EPI_F32_STORE) {
     *(float4*)((float*)Cv + i) = v;
   } else {
     E* C = (E*)Cv;
-    if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RESID || EPI == EPI_BIAS_GELU) {
-      const float4 b = *(const float4*)(p.bias + n);
+    if constexpr (epi_has_bias(EPI)) {
       v.x += b.x; v.y += b.y; v.z += b.z; v.w += b.w;
     }
     if constexpr (EPI == EPI_BIAS_RESID) {
-      const float4 r = ld4((const E*)p.resid + (long)m * p.ld_resid + n);
+      const float4 r = cvt4(in.raw);
       v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
     }
     if constexpr (EPI == EPI_GELU_BWD) {
-      const float4 u = ld4((const E*)p.aux + (long)m * p.ld_aux + n);
+      const float4 u = cvt4(in.raw);
       v.x *= gelu_grad_f(u.x); v.y *= gelu_grad_f(u.y); v.z *= gelu_grad_f(u.z); v.w *= gelu_grad_f(u.w);
     }
     st4(C + i, v);

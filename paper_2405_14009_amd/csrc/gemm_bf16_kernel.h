@@ -195,27 +195,55 @@ __device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][TN], const char* ta, c
 // padded by 8 floats so the two half-waves hit disjoint banks), then re-reads
 // it row by row so each lane applies the epilogue to 4 consecutive columns
 // with vector global accesses.  `sm` is this wave's private LDS region.
+// Epilogues with a per-element input (residual, GeLU input, gradient being
+// accumulated) fetch the next block-row's inputs while the current one is
+// finished, so those loads overlap instead of each costing a round trip.
 template <int EPI, int TN, int I0, int I1>
 __device__ __forceinline__ void epilogue(const GemmParams& p, f32x16 (&acc)[4][TN], float* sm, int m0,
                                          int n0, int lane, long c_off) {
   constexpr int COLS = 32 * TN, STRIDE = COLS + 8;
+  constexpr int NQ = COLS / 8;  // 4-column groups per lane per block-row
+  constexpr bool IN = EpiIn<EPI>::kHas;
   typedef typename EpiOut<EPI, bf16>::type OutT;
   void* C = (OutT*)p.C + c_off;
+  static_assert(64 % (COLS / 4) == 0, "a lane keeps its columns on every row");
+  float4 bias = make_float4(0.f, 0.f, 0.f, 0.f);
+  if constexpr (epi_has_bias(EPI)) {
+    const int n = n0 + 4 * (lane % (COLS / 4));
+    if (n < p.N) bias = *(const float4*)(p.bias + n);
+  }
+  EpiIn<EPI> in[2][NQ];
+  auto fetch = [&](int i, EpiIn<EPI>(&dst)[NQ]) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int idx = lane + 64 * q;
+      const int m = m0 + i * 32 + idx / (COLS / 4), n = n0 + 4 * (idx % (COLS / 4));
+      if (m < p.M && n < p.N) dst[q] = epi_fetch4<EPI, bf16>(p, C, m, n);
+    }
+  };
+  if constexpr (IN) fetch(I0, in[0]);
 #pragma unroll
   for (int i = I0; i < I1; ++i) {
+    const int cur = (i - I0) & 1;
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
         sm[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * STRIDE + 32 * j + (lane & 31)] = acc[i][j][r];
     __builtin_amdgcn_wave_barrier();
-#pragma unroll 2
-    for (int q = 0; q < COLS / 8; ++q) {
+    // The next block-row's inputs are requested once this row's accumulators
+    // are in LDS (their registers are free by then).
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (IN) {
+      if (i + 1 < I1) fetch(i + 1, in[cur ^ 1]);
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
       const int idx = lane + 64 * q;
       const int row = idx / (COLS / 4), c4 = idx % (COLS / 4);
       const float4 v = *(const float4*)(sm + row * STRIDE + 4 * c4);
       const int m = m0 + i * 32 + row, n = n0 + 4 * c4;
-      if (m < p.M && n < p.N) epi_store4<EPI, bf16>(p, C, m, n, v);
+      if (m < p.M && n < p.N) epi_finish4<EPI, bf16>(p, C, m, n, v, in[cur][q], bias);
     }
     __builtin_amdgcn_wave_barrier();
   }
