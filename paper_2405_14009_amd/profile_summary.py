@@ -45,7 +45,9 @@ def sources_digest() -> str:
 
 
 def kernel_class(name: str) -> str:
-    m = re.search(r"gemm_bf16_kernel<\s*\d+,\s*\d+,\s*\d+,\s*(true|false),\s*(true|false),\s*(\d+)", name)
+    # both bf16 GEMM kernels end their template arguments with (A k-contiguous,
+    # B k-contiguous, epilogue)
+    m = re.search(r"gemm_bf16(?:_pp)?_kernel<[^>]*?(true|false),\s*(true|false),\s*(\d+)>", name)
     if m:
         ak, bk, epi = m.group(1), m.group(2), int(m.group(3))
         if (ak, bk) == ("false", "false"):
@@ -61,7 +63,7 @@ def kernel_class(name: str) -> str:
         return "attn_fwd"
     if "attn_bwd" in name or "attn_dot_k" in name:
         return "attn_bwd"
-    if "ln_fwd_k" in name or "ln_bwd_k" in name:
+    if re.search(r"ln_(fwd|bwd)(_wave)?_k", name):
         return "layernorm"
     if "colsum" in name:
         return "reduce"
