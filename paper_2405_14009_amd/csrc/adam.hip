@@ -8,6 +8,16 @@ namespace {
 
 constexpr int NT = 256;
 
+// The update lr m_hat / (sqrt(v_hat) + eps) from the new moments.  Hardware
+// square root and reciprocal (1 ulp each; the update is 1e-4 of a weight, so
+// their error stays far below fp32 resolution of the weight).  The rollback
+// recomputes it with this same function from the same moments, so it
+// subtracts exactly what the step added.
+__device__ __forceinline__ float adam_update(float m, float v, float eps, float step_size,
+                                             float inv_sqrt_bc2) {
+  return step_size * m * __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(v) * inv_sqrt_bc2 + eps);
+}
+
 __device__ __forceinline__ float adam_one(float p, float g, float& m, float& v, bool decay,
                                           float lr, float b1, float b2, float eps, float wd,
                                           float step_size, float inv_sqrt_bc2, float gs) {
@@ -15,7 +25,13 @@ __device__ __forceinline__ float adam_one(float p, float g, float& m, float& v, 
   m = b1 * m + (1.f - b1) * g;
   v = b2 * v + (1.f - b2) * g * g;
   if (decay) p *= (1.f - lr * wd);
-  return p - step_size * m / (sqrtf(v) * inv_sqrt_bc2 + eps);
+  return p - adam_update(m, v, eps, step_size, inv_sqrt_bc2);
+}
+
+// bf16 working copy of 4 consecutive weights: one 8-byte store.
+__device__ __forceinline__ void store_bf16x4(bf16* o, float4 w) {
+  const bf16 t[4] = {(bf16)w.x, (bf16)w.y, (bf16)w.z, (bf16)w.w};
+  *(uint2*)o = *(const uint2*)t;
 }
 
 // n and n_decay are multiples of 4 (parameter tensors are padded to 64).
@@ -34,13 +50,7 @@ __global__ __launch_bounds__(NT) void adamw_k(float4* __restrict__ p, const floa
     p[i] = pp;
     m[i] = mm;
     v[i] = vv;
-    if (wb != nullptr && dec) {
-      bf16* o = wb + 4 * i;
-      o[0] = (bf16)pp.x;
-      o[1] = (bf16)pp.y;
-      o[2] = (bf16)pp.z;
-      o[3] = (bf16)pp.w;
-    }
+    if (wb != nullptr && dec) store_bf16x4(wb + 4 * i, pp);
   }
 }
 
@@ -53,7 +63,7 @@ __device__ __forceinline__ float adam_undo(float p, float g, float& m, float& v,
                                            float lr, float b1, float b2, float eps, float wd,
                                            float step_size, float inv_sqrt_bc2, float gs, bool first) {
   g *= gs;
-  p += step_size * m / (sqrtf(v) * inv_sqrt_bc2 + eps);
+  p += adam_update(m, v, eps, step_size, inv_sqrt_bc2);
   if (decay) p /= (1.f - lr * wd);
   v = first ? 0.f : fmaxf((v - (1.f - b2) * g * g) / b2, 0.f);
   m = first ? 0.f : (m - (1.f - b1) * g) / b1;
@@ -76,13 +86,7 @@ __global__ __launch_bounds__(NT) void adamw_undo_k(float4* __restrict__ p, const
     p[i] = pp;
     m[i] = mm;
     v[i] = vv;
-    if (wb != nullptr && dec) {
-      bf16* o = wb + 4 * i;
-      o[0] = (bf16)pp.x;
-      o[1] = (bf16)pp.y;
-      o[2] = (bf16)pp.z;
-      o[3] = (bf16)pp.w;
-    }
+    if (wb != nullptr && dec) store_bf16x4(wb + 4 * i, pp);
   }
 }
 

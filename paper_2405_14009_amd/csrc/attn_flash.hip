@@ -225,6 +225,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   f32x16 o[HD / 32];
 #pragma unroll
   for (int b = 0; b < HD / 32; ++b) zero(o[b]);
+  // Reference maximum (base-2 scaled score units); the first key block always
+  // moves it, and every query's row keeps its diagonal key, so it is finite
+  // after the first block a query takes part in.
   float m_run = -1e30f, l_run = 0.f;
 
   const int nkb_all = (p.s + 63) / 64;
@@ -247,37 +250,45 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
       for (int j = 0; j < 2; ++j) sc[j] = mfma(rd_row(kt, ro, j, ks), qf[ks], sc[j]);
     const bool need_mask = (CAUSAL && k0 + 63 > q0) || (k0 + 64 > p.s);
-    float mx = -1e30f;
+    // Row maximum over the raw scores (the scale is positive), masked keys at
+    // -inf; the scale is folded into the exponent's FMA below.
+    float mx = -INFINITY;
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        float x = sc[j][r] * p.sl2;
         if (need_mask) {
           const int key = k0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          if (key >= p.s || (CAUSAL && key > qq)) x = -INFINITY;
+          if (key >= p.s || (CAUSAL && key > qq)) sc[j][r] = -INFINITY;
         }
-        sc[j][r] = x;
-        mx = fmaxf(mx, x);
+        mx = fmaxf(mx, sc[j][r]);
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.sl2;
+    // Lazy rescaling: the reference maximum m_run moves only when a row's
+    // maximum exceeds it by more than 8 (base 2), so most key blocks skip
+    // rescaling O and the row sum.  Exponentials are then at most 2^8, and
+    // O / l and the log-sum-exp are unchanged in exact arithmetic.
+    const bool grow = mx > m_run + 8.f;
+    if (__any(grow)) {
+      const float m_new = grow ? mx : m_run;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int b = 0; b < HD / 32; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[b][r] *= alpha;
+    }
     float ls = 0.f;
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(sc[j][r] - m_new);
+        const float e = __builtin_amdgcn_exp2f(fmaf(sc[j][r], p.sl2, -m_run));
         sc[j][r] = e;
         ls += e;
       }
-    l_run = l_run * alpha + ls;
-#pragma unroll
-    for (int b = 0; b < HD / 32; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[b][r] *= alpha;
+    l_run += ls;
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const bf16x8 pf = pack_frag(sc, t);

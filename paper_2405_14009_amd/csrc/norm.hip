@@ -181,12 +181,31 @@ __global__ __launch_bounds__(NT) void ln_fwd_wave_k(const E* __restrict__ x, con
   const int lane = threadIdx.x & 63, nc = h / EPC;
   const E* xr = x + row * h;
   uint4 v[MAXC];
-  float s = 0.f;
+  // For rows of up to 8 chunks per lane gamma and beta are requested with the
+  // row, not after its reductions (one wave per row and a single round of
+  // waves: a later request adds a whole memory round trip to the kernel);
+  // longer rows have no registers to spare for them.
+  constexpr bool PRE = MAXC <= 8;
+  float gg[PRE ? MAXC : 1][EPC], bb[PRE ? MAXC : 1][EPC];
+  auto ld_gb = [&](int q, int c, float (&gq)[EPC], float (&bq)[EPC]) {
+#pragma unroll
+    for (int e = 0; e < EPC; e += 4) {
+      *(float4*)(gq + e) = *(const float4*)(g + (long)c * EPC + e);
+      *(float4*)(bq + e) = *(const float4*)(b + (long)c * EPC + e);
+    }
+  };
 #pragma unroll
   for (int q = 0; q < MAXC; ++q) {
     const int c = lane + 64 * q;
     if (c < nc) {
       v[q] = *(const uint4*)(xr + (long)c * EPC);
+      if constexpr (PRE) ld_gb(q, c, gg[q], bb[q]);
+    }
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int q = 0; q < MAXC; ++q) {
+    if (lane + 64 * q < nc) {
       float f[EPC];
       unpack(v[q], (const E*)nullptr, f);
 #pragma unroll
@@ -210,15 +229,12 @@ __global__ __launch_bounds__(NT) void ln_fwd_wave_k(const E* __restrict__ x, con
   for (int q = 0; q < MAXC; ++q) {
     const int c = lane + 64 * q;
     if (c < nc) {
-      float f[EPC], gg[EPC], bb[EPC];
+      float f[EPC];
       unpack(v[q], (const E*)nullptr, f);
+      const int qi = PRE ? q : 0;
+      if constexpr (!PRE) ld_gb(q, c, gg[0], bb[0]);
 #pragma unroll
-      for (int e = 0; e < EPC; e += 4) {
-        *(float4*)(gg + e) = *(const float4*)(g + (long)c * EPC + e);
-        *(float4*)(bb + e) = *(const float4*)(b + (long)c * EPC + e);
-      }
-#pragma unroll
-      for (int e = 0; e < EPC; ++e) f[e] = (f[e] - mu) * rs * gg[e] + bb[e];
+      for (int e = 0; e < EPC; ++e) f[e] = (f[e] - mu) * rs * gg[qi][e] + bb[qi][e];
       *(uint4*)(yr + (long)c * EPC) = pack(f, (const E*)nullptr);
     }
   }
@@ -240,22 +256,41 @@ __global__ __launch_bounds__(NT) void ln_bwd_wave_k(const E* __restrict__ dout, 
   if (row >= rows) return;
   const int lane = threadIdx.x & 63, nc = h / EPC;
   const float mu = mean[row], rs = rstd[row];
-  uint4 dv[MAXC], xv[MAXC];
-  float s1 = 0.f, s2 = 0.f;
+  // For rows of up to 8 chunks per lane every input of the row (the residual
+  // and gamma too) is requested before the reductions, so the kernel pays one
+  // memory round trip, not two; longer rows load them where they are used.
+  constexpr bool PRE = MAXC <= 8;
+  uint4 dv[MAXC], xv[MAXC], rv[PRE ? MAXC : 1];
+  float gg[PRE ? MAXC : 1][EPC];
+  auto ld_g = [&](int c, float (&gq)[EPC]) {
+#pragma unroll
+    for (int e = 0; e < EPC; e += 4) *(float4*)(gq + e) = *(const float4*)(g + (long)c * EPC + e);
+  };
 #pragma unroll
   for (int q = 0; q < MAXC; ++q) {
     const int c = lane + 64 * q;
     if (c < nc) {
       dv[q] = *(const uint4*)(dout + row * h + (long)c * EPC);
       xv[q] = *(const uint4*)(x + row * h + (long)c * EPC);
-      float d[EPC], xx[EPC], gg[EPC];
+      if constexpr (PRE) {
+        rv[q] = *(const uint4*)(resid + row * h + (long)c * EPC);
+        ld_g(c, gg[q]);
+      }
+    }
+  }
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int q = 0; q < MAXC; ++q) {
+    const int c = lane + 64 * q;
+    if (c < nc) {
+      float d[EPC], xx[EPC];
       unpack(dv[q], (const E*)nullptr, d);
       unpack(xv[q], (const E*)nullptr, xx);
-#pragma unroll
-      for (int e = 0; e < EPC; e += 4) *(float4*)(gg + e) = *(const float4*)(g + (long)c * EPC + e);
+      const int qi = PRE ? q : 0;
+      if constexpr (!PRE) ld_g(c, gg[0]);
 #pragma unroll
       for (int e = 0; e < EPC; ++e) {
-        const float dz = d[e] * gg[e];
+        const float dz = d[e] * gg[qi][e];
         s1 += dz;
         s2 += dz * (xx[e] - mu) * rs;
       }
@@ -266,16 +301,20 @@ __global__ __launch_bounds__(NT) void ln_bwd_wave_k(const E* __restrict__ dout, 
   for (int q = 0; q < MAXC; ++q) {
     const int c = lane + 64 * q;
     if (c < nc) {
-      float d[EPC], xx[EPC], gg[EPC], r[EPC];
+      float d[EPC], xx[EPC], r[EPC];
       unpack(dv[q], (const E*)nullptr, d);
       unpack(xv[q], (const E*)nullptr, xx);
-      unpack(*(const uint4*)(resid + row * h + (long)c * EPC), (const E*)nullptr, r);
-#pragma unroll
-      for (int e = 0; e < EPC; e += 4) *(float4*)(gg + e) = *(const float4*)(g + (long)c * EPC + e);
+      const int qi = PRE ? q : 0;
+      if constexpr (PRE) {
+        unpack(rv[q], (const E*)nullptr, r);
+      } else {
+        unpack(*(const uint4*)(resid + row * h + (long)c * EPC), (const E*)nullptr, r);
+        ld_g(c, gg[0]);
+      }
 #pragma unroll
       for (int e = 0; e < EPC; ++e) {
         const float xh = (xx[e] - mu) * rs;
-        r[e] += rs * (d[e] * gg[e] - m1 - xh * m2);
+        r[e] += rs * (d[e] * gg[qi][e] - m1 - xh * m2);
       }
       *(uint4*)(dx + row * h + (long)c * EPC) = pack(r, (const E*)nullptr);
     }
