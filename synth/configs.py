@@ -105,6 +105,13 @@ TEST_CONFIGS = {
         name="small_f32", layers=2, hidden=192, heads=3, ffn=768, seq=136, micro_batch=2,
         causal=True, dtype="f32", n_mb=3, rerouted=(2,), schedule="1f1b_deferred_shuffled_w",
         warmup=2, perturbed=True),
+    # A wide FFN makes the FC1 forward, FC2 input-gradient and FC1/FC2 weight
+    # products large enough to take 256 x 256 GEMM tiles, with ragged edges
+    # (640 tokens = 2.5 tiles, hidden 1152 = 4.5 tiles).
+    "wide_bf16": StageConfig(
+        name="wide_bf16", layers=1, hidden=1152, heads=9, ffn=12288, seq=320, micro_batch=2,
+        causal=True, dtype="bf16", n_mb=2, rerouted=(1,), schedule="1f1b_deferred_shuffled_w",
+        warmup=2, perturbed=True),
     "tiny_noncausal": CONFIGS["tiny"].with_(name="tiny_noncausal", causal=False),
     "tiny_perturbed": CONFIGS["tiny"].with_(name="tiny_perturbed", perturbed=True),
 }

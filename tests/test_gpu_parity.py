@@ -79,7 +79,8 @@ def check_adam_on_gpu_grads(cfg, g, params0, hp=None):
             assert rel_l2(g.m[l][p], M) < 1e-6 and rel_l2(g.v[l][p], V) < 1e-5, (l, p)
 
 
-@pytest.mark.parametrize("name", ["tiny", "tiny_noncausal", "tiny_perturbed", "small_f32", "small_bf16"])
+@pytest.mark.parametrize("name", ["tiny", "tiny_noncausal", "tiny_perturbed", "small_f32", "small_bf16",
+                                  "wide_bf16"])
 def test_elementwise_parity(name):
     cfg = get_config(name)
     log(f"[parity] {name}: shapes L={cfg.layers} h={cfg.hidden} a={cfg.heads} f={cfg.ffn} "
