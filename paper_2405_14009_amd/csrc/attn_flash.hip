@@ -128,6 +128,39 @@ __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Two independent MFMA chains over the head dimension: a0 += rows of block
+// b0 of tile t0 times s0, a1 += rows of block b1 of tile t1 times s1 (the
+// stationary operands in registers).  The fragments of k-step ks + D are read
+// while the MFMAs of ks issue, so LDS latency hides behind D k-steps of
+// matrix work instead of stalling every step.
+template <int D>
+__device__ __forceinline__ void two_chains(f32x16& a0, const char* t0, int b0, const bf16x8 (&s0)[HD / 16],
+                                           f32x16& a1, const char* t1, int b1, const bf16x8 (&s1)[HD / 16],
+                                           const RowOffs& ro) {
+  constexpr int NK = HD / 16, NB = D + 1;
+  bf16x8 f[NB][2];
+#pragma unroll
+  for (int i = 0; i < D; ++i) {
+    f[i][0] = rd_row(t0, ro, b0, i);
+    f[i][1] = rd_row(t1, ro, b1, i);
+  }
+  // scheduling groups pin the order (otherwise the scheduler sinks each read
+  // next to its MFMA to save registers): D k-steps of reads, then per k-step
+  // the next reads followed by this step's two MFMAs
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * D, 0);
+#pragma unroll
+  for (int ks = 0; ks < NK; ++ks) {
+    if (ks + D < NK) {
+      f[(ks + D) % NB][0] = rd_row(t0, ro, b0, ks + D);
+      f[(ks + D) % NB][1] = rd_row(t1, ro, b1, ks + D);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+    a0 = mfma(f[ks % NB][0], s0[ks], a0);
+    a1 = mfma(f[ks % NB][1], s1[ks], a1);
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+  }
+}
+
 // B fragment of 16-token step t from a pair of score blocks (32 tokens each):
 // elements r = 8 (t % 2) .. +7 of block t / 2, rounded to bf16.
 __device__ __forceinline__ bf16x8 pack_frag(const f32x16 (&p)[2], int t) {
@@ -245,10 +278,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     f32x16 sc[2];
     zero(sc[0]);
     zero(sc[1]);
-#pragma unroll
-    for (int ks = 0; ks < HD / 16; ++ks)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) sc[j] = mfma(rd_row(kt, ro, j, ks), qf[ks], sc[j]);
+    two_chains<2>(sc[0], kt, 0, qf, sc[1], kt, 1, qf, ro);
     const bool need_mask = (CAUSAL && k0 + 63 > q0) || (k0 + 64 > p.s);
     // Row maximum over the raw scores (the scale is positive), masked keys at
     // -inf; the scale is folded into the exponent's FMA below.
@@ -408,11 +438,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_k(AttnArgs p) {
       f32x16 sc, dp;
       zero(sc);
       zero(dp);
-#pragma unroll
-      for (int ks = 0; ks < HD / 16; ++ks) {
-        sc = mfma(rd_row(qt, ro, j, ks), kf[ks], sc);
-        dp = mfma(rd_row(ot, ro, j, ks), vf[ks], dp);
-      }
+      two_chains<2>(sc, qt, j, kf, dp, ot, j, vf, ro);
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
         const int ql = 32 * j + 8 * rg + 4 * (lane >> 5);
@@ -518,11 +544,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       f32x16 sc, dp;
       zero(sc);
       zero(dp);
-#pragma unroll
-      for (int ks = 0; ks < HD / 16; ++ks) {
-        sc = mfma(rd_row(kt, ro, j, ks), qf[ks], sc);
-        dp = mfma(rd_row(vt, ro, j, ks), of[ks], dp);
-      }
+      two_chains<2>(sc, kt, j, qf, dp, vt, j, of, ro);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         float pv = __builtin_amdgcn_exp2f(sc[r] * p.sl2 - Lq);
