@@ -48,6 +48,16 @@ struct GemmParams {
   const void* aux; long ld_aux;
   void* C2; long ldc2;
   int accumulate;
+  // Column sums of B over k (bf16 GEMMs with A and B m/n-contiguous): the
+  // bias gradient of a linear layer is exactly this sum of its output
+  // gradient, the B operand of its weight-gradient product.  The workgroup of
+  // tile-row tm sums the B tiles it stages anyway whose k-tile index t has
+  // t mod tiles_m == tm, into row tm of colsum_work (gemm_colsum_floats
+  // floats); a second kernel adds the rows in a fixed order and writes
+  // (colsum_acc: adds) them to colsum_out[0, N) in fp32.  nullptr: off.
+  float* colsum_out;
+  int colsum_acc;
+  float* colsum_work;
   // Reduction split into segments of kseg_len (0: one segment).  Segment s
   // of A / B starts at segA[s] / segB[s] (A, B are ignored); within a segment
   // the layouts above apply with k counted from the segment start.  Used to
@@ -61,6 +71,9 @@ struct GemmParams {
 // Shapes must satisfy: M, N, K multiples of 8 when an operand is loaded
 // along that dimension in 8-element vectors (checked by the caller).
 hipError_t gemm_bf16(const GemmParams& p, hipStream_t s);
+// Floats of colsum_work a bf16 GEMM of M rows and N columns needs (its
+// tile-rows are 256 high).
+inline long gemm_colsum_floats(long M, long N) { return ((M + 255) / 256) * N; }
 hipError_t gemm_f32(const GemmParams& p, hipStream_t s);
 
 template <int EPI, class E>

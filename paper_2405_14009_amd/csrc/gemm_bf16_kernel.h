@@ -101,6 +101,55 @@ struct Copier {
   }
 };
 
+// Column sums over k of the staged m/n-contiguous B tiles ([BK][BN] bf16,
+// 16-byte chunks swizzled by k-row), accumulated over the k-tiles a
+// workgroup takes part for: thread t (of 512) owns chunk column t % (BN / 8)
+// and k-rows t / (BN / 8) + R i of every tile (R row groups), 8 fp32 partial
+// sums.  finish() adds the R partials of each column in a fixed order through
+// LDS and stores the workgroup's row of partial sums, so the result is
+// reproducible.
+template <int BN, int BK>
+struct ColSums {
+  static constexpr int CC = BN / 8, R = 512 / CC, RPT = BK / R;
+  static_assert(BK % R == 0, "row groups");
+  static constexpr int RED_BYTES = R * BN * 4;
+  float s[8];
+  int cc, rg;
+  __device__ __forceinline__ void init(int tid) {
+    cc = tid % CC;
+    rg = tid / CC;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e] = 0.f;
+  }
+  __device__ __forceinline__ void tile(const char* tb) {
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      const int k = rg + R * i;
+      const uint4 v = *(const uint4*)(tb + k * (BN * 2) + ((cc ^ swz_mn(k)) << 4));
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s[2 * e] += __uint_as_float(w[e] << 16);
+        s[2 * e + 1] += __uint_as_float(w[e] & 0xffff0000u);
+      }
+    }
+  }
+  // red: RED_BYTES of LDS that no wave touches meanwhile; every wave calls it.
+  __device__ __forceinline__ void finish(float* red, const GemmParams& p, int tm, int n0, int tid) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) red[rg * BN + 8 * cc + e] = s[e];
+    __syncthreads();
+    if (tid < BN) {
+      float t = 0.f;
+#pragma unroll 8
+      for (int r = 0; r < R; ++r) t += red[r * BN + tid];
+      const int n = n0 + tid;
+      if (n < p.N) p.colsum_work[(long)tm * p.N + n] = t;
+    }
+    __syncthreads();
+  }
+};
+
 // Per-lane byte offsets of a wave's MFMA fragments in a staged operand tile.
 // k-contiguous: off[ks] for k-step ks (block i of 32 rows adds 64 BK i).
 // m/n-contiguous: off[b] for 32-row block b (k-step ks adds 16 ks rows of
@@ -354,6 +403,14 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  // column sums of B (a workgroup-uniform condition)
+  constexpr bool CS = !AK && !BKC;  // weight-gradient layout only
+  // Every tile-row takes part in the column sums for one k-tile in tiles_m, so
+  // the extra work spreads evenly over the launch.
+  const bool cs_on = CS && p.colsum_out != nullptr && z == 0;
+  int cs_next = tm;  // next k-tile this workgroup sums
+  ColSums<BN, BK> cs;
+  if (cs_on) cs.init(threadIdx.x);
 
   // With a segmented reduction the k-tile's segment selects the operand bases
   // (a k-tile never straddles segments).
@@ -388,6 +445,14 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
     if (t + NST - 1 < nk) issue(lds + si * STAGE, kb + (t + NST - 1) * BK);
     const char* st = lds + sc * STAGE;
     mma_tile<BM, BN, AK, BKC, TN, NKS, BK>(acc, st, st + A_BYTES, fa, fb);
+    if constexpr (CS) {
+      // while the tile's MFMAs drain; the stage stays valid until the next barrier
+      __builtin_amdgcn_sched_barrier(0);
+      if (cs_on && t == cs_next) {
+        cs.tile(st + A_BYTES);
+        cs_next += tiles_m;
+      }
+    }
     sc = sc + 1 == NST ? 0 : sc + 1;
     si = si + 1 == NST ? 0 : si + 1;
   }
@@ -395,6 +460,10 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
   // LDS is free once every wave is past its last k-tile.
   __builtin_amdgcn_sched_barrier(0);
   __syncthreads();
+  static_assert(ColSums<BN, BK>::RED_BYTES <= LDS_BYTES, "column-sum reduction fits LDS");
+  if constexpr (CS) {
+    if (cs_on) cs.finish((float*)lds, p, tm, n0, threadIdx.x);
+  }
   if constexpr (KS == 2) {
     float* mine = (float*)(lds + wave * SLOT);
     float* theirs = (float*)(lds + ((1 - kg) * NWS + ws) * SLOT);
@@ -540,6 +609,14 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  // column sums of B (a workgroup-uniform condition)
+  constexpr bool CS = !AK && !BKC;  // weight-gradient layout only
+  // Every tile-row takes part in the column sums for one k-tile in tiles_m, so
+  // the extra work spreads evenly over the launch.
+  const bool cs_on = CS && p.colsum_out != nullptr && z == 0;
+  int cs_next = tm;  // next k-tile this workgroup sums
+  ColSums<BN, BK> cs;
+  if (cs_on) cs.init(threadIdx.x);
 
   auto issue = [&](char* st, int k0) {
     if (p.kseg_len > 0) {
@@ -579,6 +656,12 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
       // memory phase
       if (u == 0 && t + NST - 1 < nk) issue(lds + si * STAGE, kb + (t + NST - 1) * BK);
       load_unit<BM, BN, AK, BKC, TN, NKS, BK>(af, bfr, st, st + A_BYTES, fa, fb, u);
+      if constexpr (CS) {
+        if (u == 0 && cs_on && t == cs_next) {
+          cs.tile(st + A_BYTES);
+          cs_next += tiles_m;
+        }
+      }
       __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the unit's fragments are in registers
       if (grp == 1 && u == U - 1) wait_next(t);
       phase_barrier();
@@ -594,6 +677,10 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
 
   // LDS is free once every wave is past its last k-tile.
   __syncthreads();
+  static_assert(ColSums<BN, BK>::RED_BYTES <= LDS_BYTES, "column-sum reduction fits LDS");
+  if constexpr (CS) {
+    if (cs_on) cs.finish((float*)lds, p, tm, n0, threadIdx.x);
+  }
   if constexpr (KS == 2) {
     float* mine = (float*)(lds + wave * SLOT);
     float* theirs = (float*)(lds + ((1 - kg) * NWS + ws) * SLOT);

@@ -22,6 +22,9 @@ hipError_t gemm_bf16(const GemmParams& p, hipStream_t s) {
                          p.krange != KR_FULL))
     return hipErrorInvalidValue;
   if (p.a_kcontig && !p.b_kcontig) return gemm_bf16_nn(p, s);
+  // column sums of B: weight-gradient layout only, with its workspace
+  if (p.colsum_out != nullptr && (p.a_kcontig || p.b_kcontig || p.colsum_work == nullptr || p.batch * p.heads != 1))
+    return hipErrorInvalidValue;
   if (p.a_kcontig && p.b_kcontig) return gemm_bf16_nt(p, s);
   if (!p.a_kcontig && !p.b_kcontig) return gemm_bf16_tn(p, s);
   return hipErrorInvalidValue;

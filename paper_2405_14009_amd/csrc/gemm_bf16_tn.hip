@@ -3,10 +3,29 @@
 // buffers) and the attention products P^T dO, dS^T Q.
 #include "gemm_bf16_kernel.h"
 
+namespace {
+
+// out[n] (+)= sum over the rows r of work[r][n], in row order.
+__global__ __launch_bounds__(256) void colsum_rows_k(const float* __restrict__ work, int rows, int n,
+                                                     float* __restrict__ out, int accumulate) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= n) return;
+  float t = 0.f;
+  for (int r = 0; r < rows; ++r) t += work[(long)r * n + c];
+  out[c] = (accumulate ? out[c] : 0.f) + t;
+}
+
+}  // namespace
+
 hipError_t gemm_bf16_tn(const GemmParams& p, hipStream_t s) {
+  hipError_t e;
   switch (p.epi) {
-    case EPI_STORE: return launch_bf16<false, false, EPI_STORE>(p, s);
-    case EPI_F32_ACC: return launch_bf16<false, false, EPI_F32_ACC>(p, s);
+    case EPI_STORE: e = launch_bf16<false, false, EPI_STORE>(p, s); break;
+    case EPI_F32_ACC: e = launch_bf16<false, false, EPI_F32_ACC>(p, s); break;
     default: return hipErrorInvalidValue;
   }
+  if (e != hipSuccess || p.colsum_out == nullptr) return e;
+  hipLaunchKernelGGL(colsum_rows_k, dim3((p.N + 255) / 256), dim3(256), 0, s, p.colsum_work,
+                     (p.M + 255) / 256, p.N, p.colsum_out, p.colsum_acc);
+  return hipGetLastError();
 }

@@ -103,6 +103,7 @@ hipError_t launch_epi(const GemmParams& p, hipStream_t s) {
 hipError_t gemm_f32(const GemmParams& p, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0 || p.batch * p.heads <= 0) return hipSuccess;
   if (p.kseg_len > 0 && (p.K % p.kseg_len || p.K / p.kseg_len > GEMM_MAX_SEG)) return hipErrorInvalidValue;
+  if (p.colsum_out != nullptr) return hipErrorInvalidValue;  // bf16 products only
   if (p.a_kcontig && !p.b_kcontig) return launch_epi<true, false>(p, s);
   if (p.a_kcontig && p.b_kcontig) return launch_epi<true, true>(p, s);
   if (!p.a_kcontig && !p.b_kcontig) return launch_epi<false, false>(p, s);

@@ -75,7 +75,7 @@ struct Layout {
   WLayer w;
   FLayer fl;
   size_t wslot_bytes, fslot_bytes, off_fslots, stash_bytes;
-  size_t off_S, off_dS, off_dO, off_dv, off_check, off_part, work_bytes;
+  size_t off_S, off_dS, off_dO, off_dv, off_check, off_part, off_cswork, work_bytes;
   uint64_t acct_af, acct_sw;
 };
 
@@ -187,6 +187,10 @@ rc_status make_layout(const rc_stage_config* c, Layout& y) {
   }
   y.off_part = take(4 * colsum_part_floats(y.T, (int)std::max(3 * h, f),
                                            std::min(y.wslots, (int)GEMM_MAX_SEG)));
+  // partial bias sums of the bf16 weight-gradient products (one product at a
+  // time): the largest of [h, 3h], [h, h], [h, f], [f, h]
+  y.off_cswork = take(y.bf ? 4 * std::max(gemm_colsum_floats(h, std::max(3 * h, f)), gemm_colsum_floats(f, h))
+                           : 0);
   y.work_bytes = o;
   return RC_OK;
 }
@@ -523,21 +527,29 @@ rc_status run_backward_weight(rc_stage* st, const int* ws, int n) {
   for (int l = 0; l < y.L; ++l) {
     WPtr w[GEMM_MAX_SEG];
     for (int q = 0; q < n; ++q) w[q] = wptr(st, ws[q], l);
+    // pid: the weight; bpid: the bias of the same linear layer, whose gradient
+    // sum_t dY[t, :] the bf16 weight-gradient product computes on the side
+    // from the dY tiles it stages (the fp32 path leaves it to the column sums).
     struct {
-      int pid;
+      int pid, bpid;
       long M, N;
       char* WPtr::*X;
       char* WPtr::*dY;
-    } lin[4] = {{RC_P_W_QKV, h, 3 * h, &WPtr::A, &WPtr::dQKV},
-                {RC_P_W_O, h, h, &WPtr::O, &WPtr::dH},
-                {RC_P_W_1, h, f, &WPtr::C, &WPtr::dU},
-                {RC_P_W_2, f, h, &WPtr::G, &WPtr::dY}};
+    } lin[4] = {{RC_P_W_QKV, RC_P_B_QKV, h, 3 * h, &WPtr::A, &WPtr::dQKV},
+                {RC_P_W_O, RC_P_B_O, h, h, &WPtr::O, &WPtr::dH},
+                {RC_P_W_1, RC_P_B_1, h, f, &WPtr::C, &WPtr::dU},
+                {RC_P_W_2, RC_P_B_2, f, h, &WPtr::G, &WPtr::dY}};
     for (auto& q : lin) {
       // dW (+)= sum over the n micro-batches of X^T dY (reduction over tokens)
       if (fused) {
         GemmParams g = gp(q.M, q.N, T * n, nullptr, q.M, 0, nullptr, q.N, 0, EPI_F32_ACC,
                           gradp(st, l, q.pid), q.N);
         g.accumulate = acc;
+        if (y.bf) {
+          g.colsum_out = gradp(st, l, q.bpid);
+          g.colsum_acc = acc;
+          g.colsum_work = (float*)(st->work + y.off_cswork);
+        }
         g.kseg_len = (int)T;
         for (int k = 0; k < n; ++k) {
           g.segA[k] = w[k].*(q.X);
@@ -549,13 +561,21 @@ rc_status run_backward_weight(rc_stage* st, const int* ws, int n) {
           GemmParams g = gp(q.M, q.N, T, w[k].*(q.X), q.M, 0, w[k].*(q.dY), q.N, 0, EPI_F32_ACC,
                             gradp(st, l, q.pid), q.N);
           g.accumulate = acc || k > 0;
+          if (y.bf) {
+            g.colsum_out = gradp(st, l, q.bpid);
+            g.colsum_acc = g.accumulate;
+            g.colsum_work = (float*)(st->work + y.off_cswork);
+          }
           HIPCHK(gemm_lin(st, g, RC_K_GEMM_WGRAD));
         }
       }
     }
+    // Column sums: the LN parameters' gradients, and on the fp32 path also the
+    // biases' (bytes: n micro-batches' inputs, then the gradient update).
     const double rb = acc ? 8.0 : 4.0;
+    const double bias_in = y.bf ? 0.0 : (double)T * (6 * h + f) * E;
     Prof pr(st, RC_K_REDUCE, 0,
-            n * ((double)T * (6 * h + f) * E + 2.0 * T * h * E + 16.0 * T) + rb * (6 * h + f) + 4 * rb * h);
+            n * (bias_in + 4.0 * T * h * E + 16.0 * T) + (y.bf ? 0.0 : rb * (6 * h + f)) + 4 * rb * h);
     ColSegs sg;
     std::memset(&sg, 0, sizeof(sg));
     struct {
@@ -564,9 +584,11 @@ rc_status run_backward_weight(rc_stage* st, const int* ws, int n) {
       char* WPtr::*D;
     } bias[4] = {{RC_P_B_QKV, 3 * h, &WPtr::dQKV}, {RC_P_B_O, h, &WPtr::dH},
                  {RC_P_B_1, f, &WPtr::dU}, {RC_P_B_2, h, &WPtr::dY}};
-    for (auto& b : bias) {
-      for (int k = 0; k < n; ++k) sg.dout[k] = w[k].*(b.D);
-      HIPCHK(colsum(E, false, sg, n, b.N, T, (int)b.N, nullptr, gradp(st, l, b.pid), acc, part, s));
+    if (!y.bf) {
+      for (auto& b : bias) {
+        for (int k = 0; k < n; ++k) sg.dout[k] = w[k].*(b.D);
+        HIPCHK(colsum(E, false, sg, n, b.N, T, (int)b.N, nullptr, gradp(st, l, b.pid), acc, part, s));
+      }
     }
     for (int k = 0; k < n; ++k) {
       sg.dout[k] = w[k].dA;
