@@ -1,6 +1,6 @@
 // bf16 GEMM kernels on CDNA4 matrix cores: v_mfma_f32_32x32x16_bf16,
 // fp32 accumulate.  Two kernels share the staging and fragment machinery:
-//   gemm_bf16_kernel     256 x 256 workgroup tiles (and test variants);
+//   gemm_bf16_kernel     256 x 256 workgroup tiles;
 //   gemm_bf16_pp_kernel  256 x 128 tiles with a ping-pong schedule and a
 //                        k-split into two wave groups.
 //
@@ -45,14 +45,15 @@
 
 namespace {
 
-// k-contiguous tiles: chunk c (8 elements) of row r lives at chunk
-// c ^ swz_k<BK>(r).  Depends on r mod 32 only (so every 32-row MFMA block of
-// a wave shares it) and places the 16 rows that one ds_read_b128 pass serves
-// (16 lanes x 16 bytes) on distinct 16-byte bank groups of a 256-byte window.
+// k-contiguous tiles (64-deep k-tiles, 8 chunks of 16 bytes per row): chunk
+// c (8 elements) of row r lives at chunk c ^ swz_k<BK>(r).  Depends on r mod
+// 32 only (so every 32-row MFMA block of a wave shares it) and places the 16
+// rows that one ds_read_b128 pass serves (16 lanes x 16 bytes, two rows per
+// 256-byte window) on distinct 16-byte bank groups.
 template <int BK>
 __device__ __forceinline__ int swz_k(int r) {
-  if constexpr (BK == 64) return (r & 7) ^ ((r >> 3) & 3);  // 2 rows per window, 8 chunks
-  else return (r >> 2) & 3;                                 // 4 rows per window, 4 chunks
+  static_assert(BK == 64, "k-tiles of 64");
+  return (r & 7) ^ ((r >> 3) & 3);
 }
 // m/n-contiguous tiles: chunk c of k-row r lives at chunk c ^ swz_mn(r).
 __device__ __forceinline__ int swz_mn(int r) { return (r & 3) << 2; }
@@ -72,7 +73,7 @@ struct Copier {
   __device__ __forceinline__ void init(int wave, long ld, int mn0, int lane) {
     if (KC) {
       const int row = RPI * wave + lane / CPR;
-      kk = 8 * ((lane % CPR) ^ swz_k<BK>(row));  // the same for every slice: rows differ by 64 q or 128 q
+      kk = 8 * ((lane % CPR) ^ swz_k<BK>(row));  // the same for every slice: rows differ by 64 q
       mn = mn0 + row;
       base = (uint32_t)((long)mn * ld * 2);
     } else {
@@ -332,13 +333,13 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 template <int BM, int BN, int NW, int KS, int BK, int NST, bool AK, bool BKC, int EPI>
 __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
-  static_assert(BM == 256 && (BN == 256 || BN == 128) && NW == 8 && (KS == 1 || KS == 2) &&
-                    (BK == 32 || BK == 64) && NST >= 2, "tile shapes");
+  // the configuration the launcher uses (256 x 128 tiles run the ping-pong
+  // kernel, which owns the k-split)
+  static_assert(BM == 256 && BN == 256 && NW == 8 && KS == 1 && BK == 64 && NST >= 2, "tile shapes");
   constexpr int NWS = NW / KS;           // waves per k-group
   constexpr int WN_ = NWS / 2;           // waves along n (2 along m)
   constexpr int TN = BN / (32 * WN_);    // 32-wide blocks per wave along n
   constexpr int NKS = (BK / 16) / KS;    // k-steps per wave per k-tile
-  static_assert(NKS >= 1, "k-steps");
   constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
   constexpr int STAGE = A_BYTES + B_BYTES;
   constexpr int NA = A_BYTES / 1024, NB = B_BYTES / 1024;  // wave instructions per k-tile
@@ -346,12 +347,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
   constexpr int NIA = NA / NW, NIB = NB / NW;
   constexpr int PER_TILE = NIA + NIB;    // copy instructions per wave per k-tile
   constexpr int EPI_BYTES = 32 * (32 * TN + 8) * 4;  // one wave's epilogue block-row tile
-  // k-split reduction slots: one per wave, 2 block-rows x TN blocks x 4 KB.
-  constexpr int SLOT = 2 * TN * 4096;
-  constexpr int RED_BYTES = KS == 2 ? NW * SLOT : NW * EPI_BYTES;
-  constexpr int LDS_BYTES = NST * STAGE > RED_BYTES ? NST * STAGE : RED_BYTES;
+  constexpr int LDS_BYTES = NST * STAGE > NW * EPI_BYTES ? NST * STAGE : NW * EPI_BYTES;
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
-  static_assert(EPI_BYTES <= SLOT, "epilogue tile fits a reduction slot");
   __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
 
   const int lane = threadIdx.x & 63;
@@ -464,22 +461,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
   if constexpr (CS) {
     if (cs_on) cs.finish((float*)lds, p, tm, n0, threadIdx.x);
   }
-  if constexpr (KS == 2) {
-    float* mine = (float*)(lds + wave * SLOT);
-    float* theirs = (float*)(lds + ((1 - kg) * NWS + ws) * SLOT);
-    // The partner's slot is read only by this wave, so after the reduction it
-    // serves as this wave's epilogue tile.
-    if (kg == 0) {
-      ksplit_reduce<TN, 0>(acc, mine, theirs, lane);
-      epilogue<EPI, TN, 0, 2>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
-    } else {
-      ksplit_reduce<TN, 1>(acc, mine, theirs, lane);
-      epilogue<EPI, TN, 2, 4>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
-    }
-  } else {
-    float* sm = (float*)(lds + wave * EPI_BYTES);
-    epilogue<EPI, TN, 0, 4>(p, acc, sm, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
-  }
+  float* sm = (float*)(lds + wave * EPI_BYTES);
+  epilogue<EPI, TN, 0, 4>(p, acc, sm, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
 }
 
 // Fragments of one unit (two consecutive k-steps, 2 u and 2 u + 1 of the
@@ -542,8 +525,11 @@ __device__ __forceinline__ void phase_barrier() {
 template <int BN, int KS, int NST, int GM, bool AK, bool BKC, int EPI>
 __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
   constexpr int BM = 256, NW = 8, BK = 64;
-  static_assert((BN == 256 && KS == 1) || (BN == 128 && KS == 2), "tile shapes");
-  static_assert(NST >= 2 && (KS == 1 || NST >= 3), "a k-split group must issue a copy two phases ahead");
+  // the configuration the launcher uses: 256 x 128 tiles, two k-groups (the
+  // same schedule on 256 x 256 tiles with one k-group measured no faster than
+  // the plain kernel); a k-group issues its copy two phases ahead, so three
+  // stages at least
+  static_assert(BN == 128 && KS == 2 && NST >= 3, "tile shapes");
   constexpr int NWS = NW / KS;           // waves per k-group
   constexpr int WN_ = NWS / 2;           // waves along n (2 along m)
   constexpr int TN = BN / (32 * WN_);    // 32-wide blocks per wave along n (2)
@@ -557,7 +543,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
   constexpr int PER_TILE = NIA + NIB;
   constexpr int EPI_BYTES = 32 * (32 * TN + 8) * 4;
   constexpr int SLOT = 2 * TN * 4096;
-  constexpr int RED_BYTES = KS == 2 ? NW * SLOT : NW * EPI_BYTES;
+  constexpr int RED_BYTES = NW * SLOT;  // k-split reduction slots, one per wave
   constexpr int LDS_BYTES = NST * STAGE > RED_BYTES ? NST * STAGE : RED_BYTES;
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
   __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
@@ -681,19 +667,17 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
   if constexpr (CS) {
     if (cs_on) cs.finish((float*)lds, p, tm, n0, threadIdx.x);
   }
-  if constexpr (KS == 2) {
-    float* mine = (float*)(lds + wave * SLOT);
-    float* theirs = (float*)(lds + ((1 - kg) * NWS + ws) * SLOT);
-    if (kg == 0) {
-      ksplit_reduce<TN, 0>(acc, mine, theirs, lane);
-      epilogue<EPI, TN, 0, 2>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
-    } else {
-      ksplit_reduce<TN, 1>(acc, mine, theirs, lane);
-      epilogue<EPI, TN, 2, 4>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
-    }
+  // The partner's slot is read only by this wave, so after the reduction it
+  // serves as this wave's epilogue tile.
+  float* mine = (float*)(lds + wave * SLOT);
+  float* theirs = (float*)(lds + ((1 - kg) * NWS + ws) * SLOT);
+  static_assert(EPI_BYTES <= SLOT, "epilogue tile fits a reduction slot");
+  if (kg == 0) {
+    ksplit_reduce<TN, 0>(acc, mine, theirs, lane);
+    epilogue<EPI, TN, 0, 2>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
   } else {
-    float* sm = (float*)(lds + wave * EPI_BYTES);
-    epilogue<EPI, TN, 0, 4>(p, acc, sm, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
+    ksplit_reduce<TN, 1>(acc, mine, theirs, lane);
+    epilogue<EPI, TN, 2, 4>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
   }
 }
 
