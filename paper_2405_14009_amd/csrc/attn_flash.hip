@@ -9,8 +9,8 @@
 //             log-sum-exp (base 2, of the scaled scores) are written.
 //   backward  P is recomputed from Q, K and the stored log-sum-exp;
 //             Dv = rowsum(dO o O) (= rowsum(dP o P));  dS = P o (dP - Dv);
-//             dV = P^T dO, dK = scale dS^T Q   (kernel over key blocks), and
-//             dQ = scale dS K                  (kernel over query blocks).
+//             dQ = scale dS K, and Dv (kernel over query blocks, first), then
+//             dV = P^T dO, dK = scale dS^T Q (kernel over key blocks).
 //             Two kernels instead of atomics keep every sum in a fixed order,
 //             so the result is bitwise reproducible.
 //
@@ -346,32 +346,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   if (lane < 32 && qq < p.s) p.lse[(long)z * p.s + qq] = m_run + __builtin_amdgcn_logf(l_tot);
 }
 
-// Dv[z, q] = sum_d dO[q, d] O[q, d] for every (sequence, head, query):
-// 16 threads per row, 8 columns each.
-__global__ __launch_bounds__(256) void attn_dot_k(AttnArgs p, long rows) {
-  const long R = (long)blockIdx.x * 16 + (threadIdx.x >> 4);
-  if (R >= rows) return;
-  const int c = 8 * (threadIdx.x & 15);
-  const long tok = R / p.heads;
-  const int zh = (int)(R % p.heads);
-  const long off = tok * p.h + zh * HD + c;
-  const uint4 a = *(const uint4*)(p.dout + off);
-  const uint4 b = *(const uint4*)(p.o + off);
-  const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
-  float acc = 0.f;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    acc += __uint_as_float(av[i] << 16) * __uint_as_float(bv[i] << 16);
-    acc += __uint_as_float(av[i] & 0xffff0000u) * __uint_as_float(bv[i] & 0xffff0000u);
-  }
-#pragma unroll
-  for (int o = 8; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 16);
-  if ((threadIdx.x & 15) == 0) {
-    const long zb = tok / p.s, q = tok % p.s;
-    p.dv[(zb * p.heads + zh) * p.s + q] = acc;
-  }
-}
-
 // ---------------------------------------------------------------------------
 // Backward over key blocks: dK, dV.  Workgroup: 128 keys of one (sequence,
 // head), 4 waves x 32 keys (K and V rows stationary in registers); query
@@ -515,7 +489,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   load_stationary(qf, Q, ld, qq, p.s, lane);
   load_stationary(of, dO, p.h, qq, p.s, lane);
   const float Lq = qq < p.s ? p.lse[(long)z * p.s + qq] : 0.f;
-  const float Dq = qq < p.s ? p.dv[(long)z * p.s + qq] : 0.f;
+  // Dv = rowsum(dO o O) of this lane's query: each half-wave holds half of the
+  // row (the same columns as its dO fragments); written for the key-block
+  // kernel, which runs after this one.
+  float Dq;
+  {
+    bf16x8 ofr[HD / 16];
+    load_stationary(ofr, p.o + (long)zb * p.s * p.h + zh * HD, p.h, qq, p.s, lane);
+    float t = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < HD / 16; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t += (float)of[ks][e] * (float)ofr[ks][e];
+    Dq = t + __shfl_xor(t, 32, 64);
+    if (lane < 32 && qq < p.s) p.dv[(long)z * p.s + qq] = Dq;
+  }
   RowOffs ro;
   ro.init(lane);
   TrOffs to;
@@ -626,15 +614,14 @@ hipError_t attn_flash_backward(const void* qkv, const void* o, const void* dout,
   a.out = (bf16*)dqkv;
   a.lse = (float*)lse;
   a.dv = dv_scratch;
-  const long rows = (long)b * s * heads;
-  hipLaunchKernelGGL(attn_dot_k, dim3((unsigned)((rows + 15) / 16)), dim3(256), 0, st, a, rows);
+  // the query-block kernel also writes Dv, which the key-block kernel reads
   const dim3 grid(((s + 127) / 128) * a.bh);
   if (causal) {
-    hipLaunchKernelGGL(attn_bwd_kv_k<true>, grid, dim3(256), 0, st, a);
     hipLaunchKernelGGL(attn_bwd_q_k<true>, grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL(attn_bwd_kv_k<true>, grid, dim3(256), 0, st, a);
   } else {
-    hipLaunchKernelGGL(attn_bwd_kv_k<false>, grid, dim3(256), 0, st, a);
     hipLaunchKernelGGL(attn_bwd_q_k<false>, grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL(attn_bwd_kv_k<false>, grid, dim3(256), 0, st, a);
   }
   return hipGetLastError();
 }

@@ -61,7 +61,7 @@ def kernel_class(name: str) -> str:
         return "gemm_f32"
     if "attn_fwd_k" in name:
         return "attn_fwd"
-    if "attn_bwd" in name or "attn_dot_k" in name:
+    if "attn_bwd" in name:
         return "attn_bwd"
     if re.search(r"ln_(fwd|bwd)(_wave)?_k", name):
         return "layernorm"
