@@ -510,11 +510,10 @@ __device__ __forceinline__ void phase_barrier() {
 // other reads, and each SIMD always has one wave with MFMAs to issue: the
 // matrix core no longer idles while both waves of a SIMD sit at the same
 // barrier or wait on LDS at the same time.
-//   KS = 1 (256 x 256 tiles): group g owns rows 128 g .. 128 g + 127 (four
-//   128 x 64 wave tiles), two units per k-tile.
-//   KS = 2 (256 x 128 tiles): each group covers the whole tile with four
-//   128 x 64 wave tiles and multiplies k-steps 2 g, 2 g + 1 of every k-tile
-//   (one unit); the partial sums are added through LDS at the end.
+// Tiles are 256 x 128: each group covers the whole tile with four 128 x 64
+// wave tiles and multiplies k-steps 2 g, 2 g + 1 of every k-tile (one unit);
+// the two groups' partial sums are added through LDS at the end.  (The unit
+// loop also allows several units per k-tile, as a single k-group would need.)
 // Copies.  Tile t + NST - 1 is issued in the memory phase of tile t's first
 // unit.  Tile t + 1 is first read in group 0's first memory phase of tile
 // t + 1; before the barrier that opens that phase each wave waits for its own
