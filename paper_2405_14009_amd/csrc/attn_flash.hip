@@ -85,6 +85,21 @@ __device__ __forceinline__ void load_vec64(const i32x4& rs, char* dst, int lane,
   dma16(rs, __builtin_amdgcn_readfirstlane(lds_addr(dst)), off);
 }
 
+// Warm L2 with 32 rows (row0.., rows >= nrows skipped) of a row-major bf16
+// matrix with 128-column rows: eight copies of 4 rows into a 1 KB LDS sink
+// that nothing reads.  Issued a step before the rows are loaded into
+// registers, so that load hits L2 instead of waiting on HBM.
+__device__ __forceinline__ void warm_rows32(const i32x4& rs, char* sink, int lane, long ld, int row0,
+                                            int nrows) {
+  const int c = lane & 15;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int gr = row0 + 4 * j + (lane >> 4);
+    const uint32_t off = gr < nrows ? (uint32_t)gr * (uint32_t)(2 * ld) + 16u * c : kOOB;
+    dma16(rs, __builtin_amdgcn_readfirstlane(lds_addr(sink)), off);
+  }
+}
+
 // Row read: 32-row block starting at row 0 of the tile, k-step ks (16 of the
 // 128 columns): lane l gets row l % 32, columns 16 ks + 8 (l / 32) + 0..7.
 struct RowOffs {
@@ -193,6 +208,12 @@ __device__ __forceinline__ void load_stationary(bf16x8 (&f)[HD / 16], const bf16
   }
 }
 
+// Wait for every outstanding vector memory access of this wave.  Used after
+// loads on a rarely taken branch: the compiler otherwise carries them as
+// pending into the code after the branch and waits for them there on every
+// path, which also waits for the tile copies issued in between.
+__device__ __forceinline__ void vm_drain() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Store a [128 (d) x 32 (tokens)] accumulator set (result layout: lane column
 // = token, rows = d) as rows of a row-major bf16 matrix: 8-byte pieces.
 __device__ __forceinline__ void store_dT(const f32x16 (&acc)[HD / 32], bf16* base, long ld, int row,
@@ -225,10 +246,96 @@ __device__ __forceinline__ void block_of(const AttnArgs& p, int nblk, bool longe
 }
 
 // ---------------------------------------------------------------------------
-// Forward.  Workgroup: 128 queries of one (sequence, head), 4 waves x 32
-// queries; key blocks of 64 staged in LDS (K and V, two stages).  Per wave and
-// key block: S^T = K Q^T (16 MFMAs, Q stationary in registers), online
-// softmax per lane (= per query), O^T += V^T P^T (16 MFMAs).
+// Forward.  Per wave: 32 queries (lane column = query), Q rows stationary in
+// registers; key blocks of 64 staged in LDS (K and V).  Per wave and key
+// block: S^T = K Q^T (16 MFMAs), online softmax per lane (= per query),
+// O^T += V^T P^T (16 MFMAs).
+
+// Online-softmax state of a wave's 32 queries: unnormalised O^T, the
+// reference maximum (base-2 scaled score units) and this lane's share of the
+// row sum (lanes l and l + 32 hold the two halves of each key block's rows).
+struct FwdState {
+  f32x16 o[HD / 32];
+  float m_run, l_run;
+  // The first key block a query takes part in always moves the reference
+  // maximum, and every query's row keeps its diagonal key.
+  __device__ __forceinline__ void reset() {
+#pragma unroll
+    for (int b = 0; b < HD / 32; ++b) zero(o[b]);
+    m_run = -1e30f;
+    l_run = 0.f;
+  }
+};
+
+// One key block (keys k0..k0+63; K tile kt, V tile vt) for the wave's queries
+// q0..q0+31 (this lane's query qq).
+template <bool CAUSAL>
+__device__ __forceinline__ void fwd_block(FwdState& st, const bf16x8 (&qf)[HD / 16], const char* kt,
+                                          const char* vt, const RowOffs& ro, const TrOffs& to, int k0,
+                                          int q0, int qq, int lane, const AttnArgs& p) {
+  if (CAUSAL && k0 > q0 + 31) return;  // every key of the block is after every query of the wave
+  f32x16 sc[2];
+  zero(sc[0]);
+  zero(sc[1]);
+  two_chains<2>(sc[0], kt, 0, qf, sc[1], kt, 1, qf, ro);
+  const bool need_mask = (CAUSAL && k0 + 63 > q0) || (k0 + 64 > p.s);
+  // Row maximum over the raw scores (the scale is positive), masked keys at
+  // -inf; the scale is folded into the exponent's FMA below.
+  float mx = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      if (need_mask) {
+        const int key = k0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (key >= p.s || (CAUSAL && key > qq)) sc[j][r] = -INFINITY;
+      }
+      mx = fmaxf(mx, sc[j][r]);
+    }
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.sl2;
+  // Lazy rescaling: the reference maximum moves only when a row's maximum
+  // exceeds it by more than 8 (base 2), so most key blocks skip rescaling O
+  // and the row sum.  Exponentials are then at most 2^8, and O / l and the
+  // log-sum-exp are unchanged in exact arithmetic.
+  const bool grow = mx > st.m_run + 8.f;
+  if (__any(grow)) {
+    const float m_new = grow ? mx : st.m_run;
+    const float alpha = __builtin_amdgcn_exp2f(st.m_run - m_new);
+    st.m_run = m_new;
+    st.l_run *= alpha;
+#pragma unroll
+    for (int b = 0; b < HD / 32; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) st.o[b][r] *= alpha;
+  }
+  float ls = 0.f;
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float e = __builtin_amdgcn_exp2f(fmaf(sc[j][r], p.sl2, -st.m_run));
+      sc[j][r] = e;
+      ls += e;
+    }
+  st.l_run += ls;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const bf16x8 pf = pack_frag(sc, t);
+#pragma unroll
+    for (int b = 0; b < HD / 32; ++b) st.o[b] = mfma(rd_tr(vt, to, b, t), pf, st.o[b]);
+  }
+}
+
+// O = O~ / l and the row log-sum-exp m + log2 l of the wave's queries.
+__device__ __forceinline__ void fwd_store(const FwdState& st, const AttnArgs& p, int z, int qq, int lane) {
+  const int zb = z / p.heads, zh = z % p.heads;
+  const float l_tot = st.l_run + __shfl_xor(st.l_run, 32, 64);
+  const float inv = 1.0f / l_tot;
+  store_dT(st.o, (bf16*)p.out + (long)zb * p.s * p.h + zh * HD, p.h, qq, p.s, lane, inv);
+  if (lane < 32 && qq < p.s) p.lse[(long)z * p.s + qq] = st.m_run + __builtin_amdgcn_logf(l_tot);
+}
+
+// One query block of 128 per workgroup (4 waves), two stages of K and V.
 template <bool CAUSAL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_k(AttnArgs p) {
   __shared__ __attribute__((aligned(1024))) char lds0[2 * TILE64];
@@ -241,10 +348,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int zb = z / p.heads, zh = z % p.heads;
   const long ld = 3L * p.h;
   const bf16* Q = p.qkv + (long)zb * p.s * ld + zh * HD;
-  const bf16* K = Q + p.h;
-  const bf16* V = Q + 2 * p.h;
-  const i32x4 rk = make_rsrc(K, 2L * p.s * ld);
-  const i32x4 rv = make_rsrc(V, 2L * p.s * ld);
+  const i32x4 rk = make_rsrc(Q + p.h, 2L * p.s * ld);
+  const i32x4 rv = make_rsrc(Q + 2 * p.h, 2L * p.s * ld);
   const int q0 = qb * 128 + 32 * wave;
   const int qq = q0 + (lane & 31);
 
@@ -254,77 +359,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   ro.init(lane);
   TrOffs to;
   to.init(lane);
-
-  f32x16 o[HD / 32];
-#pragma unroll
-  for (int b = 0; b < HD / 32; ++b) zero(o[b]);
-  // Reference maximum (base-2 scaled score units); the first key block always
-  // moves it, and every query's row keeps its diagonal key, so it is finite
-  // after the first block a query takes part in.
-  float m_run = -1e30f, l_run = 0.f;
+  FwdState st;
+  st.reset();
 
   const int nkb_all = (p.s + 63) / 64;
   const int nkb = CAUSAL ? min(nkb_all, 2 * qb + 2) : nkb_all;
 
-  auto issue = [&](char* st, int kb) {
-    load_tile<64>(rk, st, wave, lane, ld, kb * 64, p.s);
-    load_tile<64>(rv, st + TILE64, wave, lane, ld, kb * 64, p.s);
+  auto issue = [&](char* t, int kb) {
+    load_tile<64>(rk, t, wave, lane, ld, kb * 64, p.s);
+    load_tile<64>(rv, t + TILE64, wave, lane, ld, kb * 64, p.s);
   };
-  auto compute = [&](const char* st, int kb) {
-    const int k0 = kb * 64;
-    if (CAUSAL && k0 > q0 + 31) return;  // every key of the block is after every query of the wave
-    const char* kt = st;
-    const char* vt = st + TILE64;
-    f32x16 sc[2];
-    zero(sc[0]);
-    zero(sc[1]);
-    two_chains<2>(sc[0], kt, 0, qf, sc[1], kt, 1, qf, ro);
-    const bool need_mask = (CAUSAL && k0 + 63 > q0) || (k0 + 64 > p.s);
-    // Row maximum over the raw scores (the scale is positive), masked keys at
-    // -inf; the scale is folded into the exponent's FMA below.
-    float mx = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        if (need_mask) {
-          const int key = k0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          if (key >= p.s || (CAUSAL && key > qq)) sc[j][r] = -INFINITY;
-        }
-        mx = fmaxf(mx, sc[j][r]);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.sl2;
-    // Lazy rescaling: the reference maximum m_run moves only when a row's
-    // maximum exceeds it by more than 8 (base 2), so most key blocks skip
-    // rescaling O and the row sum.  Exponentials are then at most 2^8, and
-    // O / l and the log-sum-exp are unchanged in exact arithmetic.
-    const bool grow = mx > m_run + 8.f;
-    if (__any(grow)) {
-      const float m_new = grow ? mx : m_run;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int b = 0; b < HD / 32; ++b)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[b][r] *= alpha;
-    }
-    float ls = 0.f;
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(sc[j][r], p.sl2, -m_run));
-        sc[j][r] = e;
-        ls += e;
-      }
-    l_run += ls;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const bf16x8 pf = pack_frag(sc, t);
-#pragma unroll
-      for (int b = 0; b < HD / 32; ++b) o[b] = mfma(rd_tr(vt, to, b, t), pf, o[b]);
-    }
+  auto compute = [&](const char* t, int kb) {
+    fwd_block<CAUSAL>(st, qf, t, t + TILE64, ro, to, kb * 64, q0, qq, lane, p);
   };
 
   if (nkb > 0) issue(lds0, 0);
@@ -339,11 +385,142 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     stage_sync();
   }
   if (kb < nkb) compute(lds0, kb);
+  fwd_store(st, p, z, qq, lane);
+}
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  const float inv = 1.0f / l_tot;
-  store_dT(o, (bf16*)p.out + (long)zb * p.s * p.h + zh * HD, p.h, qq, p.s, lane, inv);
-  if (lane < 32 && qq < p.s) p.lse[(long)z * p.s + qq] = m_run + __builtin_amdgcn_logf(l_tot);
+// Causal forward over pairs of query blocks.  Query block q needs the key
+// blocks [0, n(q)), n(q) = min(ceil(s / 64), 2 q + 2): at s = 2048 the first
+// and the last block differ 16-fold in work, and with one block per
+// workgroup some SIMDs idle while others finish long blocks.  Here a
+// workgroup of eight waves takes the blocks qa = i and qb = nqb - 1 - i
+// (n(qa) + n(qb) is about the same for every pair) and cuts the sequence of
+// steps [qa: key blocks 0..n(qa)), [qb: key blocks 0..n(qb)) in two halves:
+// waves 0-3 run the first half (all of qa, then the first key blocks of qb),
+// waves 4-7 the rest of qb.  Waves w and w + 4 share a SIMD, so every SIMD
+// carries half of the pair.  The two partial softmax states of qb (lane for
+// lane the same queries) are merged through LDS at the end.  A middle block
+// (odd nqb) pairs with itself: its key blocks are split the same way.
+constexpr int FWD_STAGE = 2 * TILE64;        // K | V of one key block
+constexpr int FWD_GROUP = 2 * FWD_STAGE;     // two stages per wave group
+
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_pair_k(AttnArgs p) {
+  __shared__ __attribute__((aligned(1024))) char lds[2 * FWD_GROUP + 1024];
+  char* const sink = lds + 2 * FWD_GROUP;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int grp = wave >> 2, wg = wave & 3;
+  const int nqb = (p.s + 127) / 128;
+  const int z = blockIdx.x % p.bh, pr = blockIdx.x / p.bh;
+  const int qa = pr, qb = nqb - 1 - pr;
+  const int nkb_all = (p.s + 63) / 64;
+  const int nb = min(nkb_all, 2 * qb + 2);
+  const int na = qa == qb ? 0 : min(nkb_all, 2 * qa + 2);
+  const int half = (na + nb + 1) / 2;
+  const int j0 = grp ? half : 0;                     // this group's first step
+  const int cnt = grp ? na + nb - half : half;       // and its number of steps
+  const int zb = z / p.heads, zh = z % p.heads;
+  const long ld = 3L * p.h;
+  const bf16* Q = p.qkv + (long)zb * p.s * ld + zh * HD;
+  const i32x4 rk = make_rsrc(Q + p.h, 2L * p.s * ld);
+  const i32x4 rv = make_rsrc(Q + 2 * p.h, 2L * p.s * ld);
+  const i32x4 rq = make_rsrc(Q, 2L * p.s * ld);
+
+  int qcur = j0 < na ? qa : qb;
+  int q0 = qcur * 128 + 32 * wg;
+  int qq = q0 + (lane & 31);
+  bf16x8 qf[HD / 16];
+  load_stationary(qf, Q, ld, qq, p.s, lane);
+  // fragment offsets carry the group's LDS base, so stage pointers stay constants
+  RowOffs ro;
+  ro.init(lane);
+  TrOffs to;
+  to.init(lane);
+#pragma unroll
+  for (int ks = 0; ks < HD / 16; ++ks) ro.off[ks] += grp * FWD_GROUP;
+#pragma unroll
+  for (int b = 0; b < HD / 32; ++b) {
+    to.off[b][0] += grp * FWD_GROUP;
+    to.off[b][1] += grp * FWD_GROUP;
+  }
+  FwdState st;
+  st.reset();
+
+  auto key_block = [&](int j) { return j < na ? j : j - na; };
+  auto issue = [&](char* t, int j) {
+    char* g = t + grp * FWD_GROUP;
+    const int kb = key_block(j);
+    load_tile<64>(rk, g, wg, lane, ld, kb * 64, p.s);
+    load_tile<64>(rv, g + TILE64, wg, lane, ld, kb * 64, p.s);
+  };
+  // step it of this group: (on moving to qb, its Q rows first, so the first
+  // products wait for them and not for the copy), the copy of the next step's
+  // tiles, then the products
+  auto step = [&](int it, const char* cur, char* nxt) {
+    const int j = j0 + it;
+    if (it < cnt && j == na && qcur != qb) {  // group 0 leaves qa: its rows are complete
+      fwd_store(st, p, z, qq, lane);
+      st.reset();
+      qcur = qb;
+      q0 = qcur * 128 + 32 * wg;
+      qq = q0 + (lane & 31);
+      load_stationary(qf, Q, ld, qq, p.s, lane);
+      vm_drain();
+    }
+    if (it < cnt && j + 1 == na) warm_rows32(rq, sink, lane, ld, qb * 128 + 32 * wg, p.s);
+    if (it + 1 < cnt) issue(nxt, j + 1);
+    if (it < cnt) fwd_block<true>(st, qf, cur, cur + TILE64, ro, to, key_block(j) * 64, q0, qq, lane, p);
+  };
+
+  if (cnt > 0) issue(lds, j0);
+  stage_sync();
+  int it = 0;
+  for (; it + 1 < half; it += 2) {
+    step(it, lds, lds + FWD_STAGE);
+    stage_sync();
+    step(it + 1, lds + FWD_STAGE, lds);
+    stage_sync();
+  }
+  if (it < half) {
+    step(it, lds, lds + FWD_STAGE);
+    stage_sync();
+  }
+
+  // Merge qb: group 0 publishes its partial state (lane-major float4 chunks,
+  // conflict-free), group 1 combines it with its own and stores.
+  if (grp == 0) {
+    if (qcur != qb) {  // no step of qb in this half: qa is complete, qb's share is empty
+      fwd_store(st, p, z, qq, lane);
+      st.reset();
+    }
+    float4* dst = (float4*)lds + wg * 16 * 64 + lane;
+#pragma unroll
+    for (int b = 0; b < HD / 32; ++b)
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        dst[(4 * b + c) * 64] = make_float4(st.o[b][4 * c], st.o[b][4 * c + 1], st.o[b][4 * c + 2],
+                                            st.o[b][4 * c + 3]);
+    ((float2*)(lds + FWD_GROUP))[wg * 64 + lane] = make_float2(st.m_run, st.l_run);
+  }
+  __syncthreads();
+  if (grp == 1) {
+    const float2 ml = ((const float2*)(lds + FWD_GROUP))[wg * 64 + lane];
+    const float m = fmaxf(ml.x, st.m_run);
+    const float a0 = __builtin_amdgcn_exp2f(ml.x - m), a1 = __builtin_amdgcn_exp2f(st.m_run - m);
+    const float4* src = (const float4*)lds + wg * 16 * 64 + lane;
+#pragma unroll
+    for (int b = 0; b < HD / 32; ++b)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const float4 v = src[(4 * b + c) * 64];
+        st.o[b][4 * c] = v.x * a0 + st.o[b][4 * c] * a1;
+        st.o[b][4 * c + 1] = v.y * a0 + st.o[b][4 * c + 1] * a1;
+        st.o[b][4 * c + 2] = v.z * a0 + st.o[b][4 * c + 2] * a1;
+        st.o[b][4 * c + 3] = v.w * a0 + st.o[b][4 * c + 3] * a1;
+      }
+    st.l_run = ml.y * a0 + st.l_run * a1;
+    st.m_run = m;
+    fwd_store(st, p, z, qq, lane);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -461,10 +638,82 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_k(AttnArgs p) {
   store_dT(dv, dK + p.h, ld, key, p.s, lane, 1.0f);
 }
 
-// Backward over query blocks: dQ.  Workgroup: 128 queries, 4 waves x 32
-// (Q and dO rows stationary); key blocks of 64 staged in LDS (K, V).  Per
-// wave and key block: S^T = K Q^T, dP^T = V dO^T (lane column = query),
-// P, dS as above; dQ^T += K^T dS^T.
+// Backward over query blocks: dQ.  Per wave: 32 queries (Q and dO rows
+// stationary in registers); key blocks of 64 staged in LDS (K, V).  Per wave
+// and key block: S^T = K Q^T, dP^T = V dO^T (lane column = query), P, dS as
+// above; dQ^T += K^T dS^T.
+
+// Stationary operands of a wave's 32 queries: Q and dO fragments, this lane's
+// query's log-sum-exp and Dv = rowsum(dO o O).  Each half-wave holds half of
+// a row (the same columns as its dO fragments); Dv is written for the
+// key-block kernel, which runs after this one.
+struct BwdQRows {
+  bf16x8 qf[HD / 16], of[HD / 16];
+  float Lq, Dq;
+  __device__ __forceinline__ void load_rows(const AttnArgs& p, int z, int qq, int lane) {
+    const int zb = z / p.heads, zh = z % p.heads;
+    const long ld = 3L * p.h;
+    load_stationary(qf, p.qkv + (long)zb * p.s * ld + zh * HD, ld, qq, p.s, lane);
+    load_stationary(of, p.dout + (long)zb * p.s * p.h + zh * HD, p.h, qq, p.s, lane);
+  }
+  __device__ __forceinline__ void load(const AttnArgs& p, int z, int qq, int lane, bool write_dv) {
+    const int zb = z / p.heads, zh = z % p.heads;
+    load_rows(p, z, qq, lane);
+    Lq = qq < p.s ? p.lse[(long)z * p.s + qq] : 0.f;
+    bf16x8 ofr[HD / 16];
+    load_stationary(ofr, p.o + (long)zb * p.s * p.h + zh * HD, p.h, qq, p.s, lane);
+    float t = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < HD / 16; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t += (float)of[ks][e] * (float)ofr[ks][e];
+    Dq = t + __shfl_xor(t, 32, 64);
+    if (write_dv && lane < 32 && qq < p.s) p.dv[(long)z * p.s + qq] = Dq;
+  }
+};
+
+// One key block (keys k0..k0+63; K tile kt, V tile vt) for the wave's queries
+// q0..q0+31.
+template <bool CAUSAL>
+__device__ __forceinline__ void bwdq_block(f32x16 (&dq)[HD / 32], const BwdQRows& w, const char* kt,
+                                           const char* vt, const RowOffs& ro, const TrOffs& to, int k0,
+                                           int q0, int qq, int lane, const AttnArgs& p) {
+  if (CAUSAL && k0 > q0 + 31) return;
+  const bool need_mask = (CAUSAL && k0 + 63 > q0) || (k0 + 64 > p.s);
+  // the two 32-key halves of the block in turn (one half's scores live)
+#pragma unroll 1
+  for (int j = 0; j < 2; ++j) {
+    if (CAUSAL && k0 + 32 * j > q0 + 31) break;  // this half is after every query of the wave
+    f32x16 sc, dp;
+    zero(sc);
+    zero(dp);
+    two_chains<2>(sc, kt, j, w.qf, dp, vt, j, w.of, ro);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float pv = __builtin_amdgcn_exp2f(sc[r] * p.sl2 - w.Lq);
+      if (need_mask) {
+        const int key = k0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (key >= p.s || (CAUSAL && key > qq)) pv = 0.f;
+      }
+      dp[r] = pv * (dp[r] - w.Dq);
+    }
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const bf16x8 sf = pack_half(dp, hf);
+#pragma unroll
+      for (int b = 0; b < HD / 32; ++b) dq[b] = mfma(rd_tr(kt, to, b, 2 * j + hf), sf, dq[b]);
+    }
+  }
+}
+
+__device__ __forceinline__ void store_dq(const f32x16 (&dq)[HD / 32], const AttnArgs& p, int z, int qq,
+                                         int lane) {
+  const int zb = z / p.heads, zh = z % p.heads;
+  const long ld = 3L * p.h;
+  store_dT(dq, p.out + (long)zb * p.s * ld + zh * HD, ld, qq, p.s, lane, p.scale);
+}
+
+// One query block of 128 per workgroup (4 waves), two stages of K and V.
 template <bool CAUSAL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_q_k(AttnArgs p) {
   __shared__ __attribute__((aligned(1024))) char lds0[2 * TILE64];
@@ -477,33 +726,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int zb = z / p.heads, zh = z % p.heads;
   const long ld = 3L * p.h;
   const bf16* Q = p.qkv + (long)zb * p.s * ld + zh * HD;
-  const bf16* K = Q + p.h;
-  const bf16* V = Q + 2 * p.h;
-  const bf16* dO = p.dout + (long)zb * p.s * p.h + zh * HD;
-  const i32x4 rk = make_rsrc(K, 2L * p.s * ld);
-  const i32x4 rv = make_rsrc(V, 2L * p.s * ld);
+  const i32x4 rk = make_rsrc(Q + p.h, 2L * p.s * ld);
+  const i32x4 rv = make_rsrc(Q + 2 * p.h, 2L * p.s * ld);
   const int q0 = qb * 128 + 32 * wave;
   const int qq = q0 + (lane & 31);
 
-  bf16x8 qf[HD / 16], of[HD / 16];
-  load_stationary(qf, Q, ld, qq, p.s, lane);
-  load_stationary(of, dO, p.h, qq, p.s, lane);
-  const float Lq = qq < p.s ? p.lse[(long)z * p.s + qq] : 0.f;
-  // Dv = rowsum(dO o O) of this lane's query: each half-wave holds half of the
-  // row (the same columns as its dO fragments); written for the key-block
-  // kernel, which runs after this one.
-  float Dq;
-  {
-    bf16x8 ofr[HD / 16];
-    load_stationary(ofr, p.o + (long)zb * p.s * p.h + zh * HD, p.h, qq, p.s, lane);
-    float t = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < HD / 16; ++ks)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) t += (float)of[ks][e] * (float)ofr[ks][e];
-    Dq = t + __shfl_xor(t, 32, 64);
-    if (lane < 32 && qq < p.s) p.dv[(long)z * p.s + qq] = Dq;
-  }
+  BwdQRows w;
+  w.load(p, z, qq, lane, true);
   RowOffs ro;
   ro.init(lane);
   TrOffs to;
@@ -515,40 +744,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int nkb_all = (p.s + 63) / 64;
   const int nkb = CAUSAL ? min(nkb_all, 2 * qb + 2) : nkb_all;
 
-  auto issue = [&](char* st, int kb) {
-    load_tile<64>(rk, st, wave, lane, ld, kb * 64, p.s);
-    load_tile<64>(rv, st + TILE64, wave, lane, ld, kb * 64, p.s);
+  auto issue = [&](char* t, int kb) {
+    load_tile<64>(rk, t, wave, lane, ld, kb * 64, p.s);
+    load_tile<64>(rv, t + TILE64, wave, lane, ld, kb * 64, p.s);
   };
-  auto compute = [&](const char* st, int kb) {
-    const int k0 = kb * 64;
-    if (CAUSAL && k0 > q0 + 31) return;
-    const char* kt = st;
-    const char* vt = st + TILE64;
-    const bool need_mask = (CAUSAL && k0 + 63 > q0) || (k0 + 64 > p.s);
-    // the two 32-key halves of the block in turn (one half's scores live)
-#pragma unroll 1
-    for (int j = 0; j < 2; ++j) {
-      if (CAUSAL && k0 + 32 * j > q0 + 31) break;  // this half is after every query of the wave
-      f32x16 sc, dp;
-      zero(sc);
-      zero(dp);
-      two_chains<2>(sc, kt, j, qf, dp, vt, j, of, ro);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float pv = __builtin_amdgcn_exp2f(sc[r] * p.sl2 - Lq);
-        if (need_mask) {
-          const int key = k0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          if (key >= p.s || (CAUSAL && key > qq)) pv = 0.f;
-        }
-        dp[r] = pv * (dp[r] - Dq);
-      }
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        const bf16x8 sf = pack_half(dp, hf);
-#pragma unroll
-        for (int b = 0; b < HD / 32; ++b) dq[b] = mfma(rd_tr(kt, to, b, 2 * j + hf), sf, dq[b]);
-      }
-    }
+  auto compute = [&](const char* t, int kb) {
+    bwdq_block<CAUSAL>(dq, w, t, t + TILE64, ro, to, kb * 64, q0, qq, lane, p);
   };
 
   if (nkb > 0) issue(lds0, 0);
@@ -563,8 +764,134 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     stage_sync();
   }
   if (kb < nkb) compute(lds0, kb);
+  store_dq(dq, p, z, qq, lane);
+}
 
-  store_dT(dq, p.out + (long)zb * p.s * ld + zh * HD, ld, qq, p.s, lane, p.scale);
+// Causal dQ over pairs of query blocks: the work split of attn_fwd_pair_k
+// (waves 0-3: all of qa, then the first key blocks of qb; waves 4-7: the rest
+// of qb).  Group 1 forms the log-sum-exp and Dv of qb's rows, writes Dv to
+// memory and leaves both in LDS for group 0, which then reloads only the Q
+// and dO rows when it moves to qb.  The two partial sums of qb's dQ are added
+// through LDS (group 0's first).
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_q_pair_k(AttnArgs p) {
+  __shared__ __attribute__((aligned(1024))) char lds[2 * FWD_GROUP + 3072];
+  float2* const stats = (float2*)(lds + 2 * FWD_GROUP);  // qb's (log-sum-exp, Dv) per [wave][lane]
+  char* const sink = lds + 2 * FWD_GROUP + 2048;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int grp = wave >> 2, wg = wave & 3;
+  const int nqb = (p.s + 127) / 128;
+  const int z = blockIdx.x % p.bh, pr = blockIdx.x / p.bh;
+  const int qa = pr, qb = nqb - 1 - pr;
+  const int nkb_all = (p.s + 63) / 64;
+  const int nb = min(nkb_all, 2 * qb + 2);
+  const int na = qa == qb ? 0 : min(nkb_all, 2 * qa + 2);
+  const int half = (na + nb + 1) / 2;
+  const int j0 = grp ? half : 0;
+  const int cnt = grp ? na + nb - half : half;
+  const int zb = z / p.heads, zh = z % p.heads;
+  const long ld = 3L * p.h;
+  const bf16* Q = p.qkv + (long)zb * p.s * ld + zh * HD;
+  const i32x4 rk = make_rsrc(Q + p.h, 2L * p.s * ld);
+  const i32x4 rv = make_rsrc(Q + 2 * p.h, 2L * p.s * ld);
+  const i32x4 rq = make_rsrc(Q, 2L * p.s * ld);
+  const i32x4 rdo = make_rsrc(p.dout + (long)zb * p.s * p.h + zh * HD, 2L * p.s * p.h);
+
+  int qcur = j0 < na ? qa : qb;
+  int q0 = qcur * 128 + 32 * wg;
+  int qq = q0 + (lane & 31);
+  BwdQRows w;
+  w.load(p, z, qq, lane, grp == 1 || qcur != qb);  // group 1 writes qb's Dv, group 0 qa's
+  if (grp == 1) stats[wg * 64 + lane] = make_float2(w.Lq, w.Dq);  // read after the first barrier
+  RowOffs ro;
+  ro.init(lane);
+  TrOffs to;
+  to.init(lane);
+#pragma unroll
+  for (int ks = 0; ks < HD / 16; ++ks) ro.off[ks] += grp * FWD_GROUP;
+#pragma unroll
+  for (int b = 0; b < HD / 32; ++b) {
+    to.off[b][0] += grp * FWD_GROUP;
+    to.off[b][1] += grp * FWD_GROUP;
+  }
+  f32x16 dq[HD / 32];
+#pragma unroll
+  for (int b = 0; b < HD / 32; ++b) zero(dq[b]);
+
+  auto key_block = [&](int j) { return j < na ? j : j - na; };
+  auto issue = [&](char* t, int j) {
+    char* g = t + grp * FWD_GROUP;
+    const int kb = key_block(j);
+    load_tile<64>(rk, g, wg, lane, ld, kb * 64, p.s);
+    load_tile<64>(rv, g + TILE64, wg, lane, ld, kb * 64, p.s);
+  };
+  // step it of this group: (on moving to qb, its rows first), the copy of the
+  // next step's tiles, then the products
+  auto step = [&](int it, const char* cur, char* nxt) {
+    const int j = j0 + it;
+    if (it < cnt && j == na && qcur != qb) {  // group 0 leaves qa: its rows are complete
+      store_dq(dq, p, z, qq, lane);
+#pragma unroll
+      for (int b = 0; b < HD / 32; ++b) zero(dq[b]);
+      qcur = qb;
+      q0 = qcur * 128 + 32 * wg;
+      qq = q0 + (lane & 31);
+      w.load_rows(p, z, qq, lane);
+      vm_drain();
+      const float2 st2 = stats[wg * 64 + lane];
+      w.Lq = st2.x;
+      w.Dq = st2.y;
+    }
+    if (it < cnt && j + 1 == na) {
+      warm_rows32(rq, sink, lane, ld, qb * 128 + 32 * wg, p.s);
+      warm_rows32(rdo, sink, lane, p.h, qb * 128 + 32 * wg, p.s);
+    }
+    if (it + 1 < cnt) issue(nxt, j + 1);
+    if (it < cnt) bwdq_block<true>(dq, w, cur, cur + TILE64, ro, to, key_block(j) * 64, q0, qq, lane, p);
+  };
+
+  if (cnt > 0) issue(lds, j0);
+  stage_sync();
+  int it = 0;
+  for (; it + 1 < half; it += 2) {
+    step(it, lds, lds + FWD_STAGE);
+    stage_sync();
+    step(it + 1, lds + FWD_STAGE, lds);
+    stage_sync();
+  }
+  if (it < half) {
+    step(it, lds, lds + FWD_STAGE);
+    stage_sync();
+  }
+
+  if (grp == 0) {
+    if (qcur != qb) {  // no step of qb in this half: qa is complete, qb's share is zero
+      store_dq(dq, p, z, qq, lane);
+#pragma unroll
+      for (int b = 0; b < HD / 32; ++b) zero(dq[b]);
+    }
+    float4* dst = (float4*)lds + wg * 16 * 64 + lane;
+#pragma unroll
+    for (int b = 0; b < HD / 32; ++b)
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        dst[(4 * b + c) * 64] = make_float4(dq[b][4 * c], dq[b][4 * c + 1], dq[b][4 * c + 2], dq[b][4 * c + 3]);
+  }
+  __syncthreads();
+  if (grp == 1) {
+    const float4* src = (const float4*)lds + wg * 16 * 64 + lane;
+#pragma unroll
+    for (int b = 0; b < HD / 32; ++b)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const float4 v = src[(4 * b + c) * 64];
+        dq[b][4 * c] = v.x + dq[b][4 * c];
+        dq[b][4 * c + 1] = v.y + dq[b][4 * c + 1];
+        dq[b][4 * c + 2] = v.z + dq[b][4 * c + 2];
+        dq[b][4 * c + 3] = v.w + dq[b][4 * c + 3];
+      }
+    store_dq(dq, p, z, qq, lane);
+  }
 }
 
 AttnArgs make_args(const void* qkv, int b, int s, int heads, int h) {
@@ -584,6 +911,31 @@ AttnArgs make_args(const void* qkv, int b, int s, int heads, int h) {
   return a;
 }
 
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] <= 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+// The paired kernels run one equal-length workgroup per CU.  They are used
+// when those workgroups fill the CUs of their last round to 90 % or more, or
+// when there are so few that every CU holds at most one anyway (a small
+// problem); otherwise the per-block kernels, whose uneven blocks the
+// hardware packs two to a CU, lose less to the last round.
+bool pair_grid_fills(long wgs) {
+  const long cus = device_cus();
+  if (2 * wgs <= cus) return true;
+  const long rounds = (wgs + cus - 1) / cus;
+  return 10 * wgs >= 9 * rounds * cus;
+}
+
 }  // namespace
 
 bool attn_flash_supported(int elt, int head_dim) { return elt == 2 && head_dim == HD; }
@@ -595,7 +947,13 @@ hipError_t attn_flash_forward(const void* qkv, void* o, float* lse, int b, int s
   AttnArgs a = make_args(qkv, b, s, heads, h);
   a.out = (bf16*)o;
   a.lse = lse;
-  const dim3 grid(((s + 127) / 128) * a.bh);
+  const int nqb = (s + 127) / 128;
+  const long pairs = (long)((nqb + 1) / 2) * a.bh;
+  if (causal && pair_grid_fills(pairs)) {
+    hipLaunchKernelGGL(attn_fwd_pair_k, dim3(pairs), dim3(512), 0, st, a);
+    return hipGetLastError();
+  }
+  const dim3 grid(nqb * a.bh);
   if (causal)
     hipLaunchKernelGGL(attn_fwd_k<true>, grid, dim3(256), 0, st, a);
   else
@@ -615,9 +973,14 @@ hipError_t attn_flash_backward(const void* qkv, const void* o, const void* dout,
   a.lse = (float*)lse;
   a.dv = dv_scratch;
   // the query-block kernel also writes Dv, which the key-block kernel reads
-  const dim3 grid(((s + 127) / 128) * a.bh);
+  const int nqb = (s + 127) / 128;
+  const long pairs = (long)((nqb + 1) / 2) * a.bh;
+  const dim3 grid(nqb * a.bh);
   if (causal) {
-    hipLaunchKernelGGL(attn_bwd_q_k<true>, grid, dim3(256), 0, st, a);
+    if (pair_grid_fills(pairs))
+      hipLaunchKernelGGL(attn_bwd_q_pair_k, dim3(pairs), dim3(512), 0, st, a);
+    else
+      hipLaunchKernelGGL(attn_bwd_q_k<true>, grid, dim3(256), 0, st, a);
     hipLaunchKernelGGL(attn_bwd_kv_k<true>, grid, dim3(256), 0, st, a);
   } else {
     hipLaunchKernelGGL(attn_bwd_q_k<false>, grid, dim3(256), 0, st, a);
