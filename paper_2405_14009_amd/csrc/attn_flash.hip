@@ -231,6 +231,35 @@ __device__ __forceinline__ void store_dT(const f32x16 (&acc)[HD / 32], bf16* bas
     }
 }
 
+// The same block through this wave's 8 KB of LDS (t): rows written as bf16
+// (16-byte chunk c of row r at chunk c ^ (r % 16), so the 32 rows of one
+// write land on distinct banks), then read back 16 bytes per lane, so each
+// store instruction writes four whole 256-byte rows instead of 16-byte pieces
+// of 32 rows.  row0 is the wave's first row (lane l holds row row0 + l % 32).
+// The LDS accesses of one wave complete in order, so no wait is needed
+// between the two halves.
+__device__ __forceinline__ void store_rows_lds(const f32x16 (&acc)[HD / 32], char* t, bf16* base, long ld,
+                                               int row0, int nrows, int lane, float mul) {
+  const int r = lane & 31, hf = lane >> 5;
+#pragma unroll
+  for (int b = 0; b < HD / 32; ++b)
+#pragma unroll
+    for (int rg = 0; rg < 4; ++rg) {
+      bf16 v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = (bf16)(acc[b][4 * rg + e] * mul);
+      const int c = 4 * b + rg;  // columns 32 b + 8 rg + 4 hf + e
+      *(uint2*)(t + r * ROWB + ((c ^ (r & 15)) << 4) + 8 * hf) = *(const uint2*)v;
+    }
+  const int c = lane & 15;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int rr = 4 * i + (lane >> 4);
+    const uint4 v = *(const uint4*)(t + rr * ROWB + ((c ^ (rr & 15)) << 4));
+    if (row0 + rr < nrows) *(uint4*)(base + (long)(row0 + rr) * ld + 8 * c) = v;
+  }
+}
+
 __device__ __forceinline__ void zero(f32x16& a) {
 #pragma unroll
   for (int r = 0; r < 16; ++r) a[r] = 0.f;
@@ -326,12 +355,18 @@ __device__ __forceinline__ void fwd_block(FwdState& st, const bf16x8 (&qf)[HD / 
   }
 }
 
-// O = O~ / l and the row log-sum-exp m + log2 l of the wave's queries.
-__device__ __forceinline__ void fwd_store(const FwdState& st, const AttnArgs& p, int z, int qq, int lane) {
+// O = O~ / l and the row log-sum-exp m + log2 l of the wave's queries
+// q0..q0+31 (this lane's qq); through LDS area t (8 KB) when given.
+__device__ __forceinline__ void fwd_store(const FwdState& st, const AttnArgs& p, int z, int q0, int qq,
+                                          int lane, char* t = nullptr) {
   const int zb = z / p.heads, zh = z % p.heads;
   const float l_tot = st.l_run + __shfl_xor(st.l_run, 32, 64);
   const float inv = 1.0f / l_tot;
-  store_dT(st.o, (bf16*)p.out + (long)zb * p.s * p.h + zh * HD, p.h, qq, p.s, lane, inv);
+  bf16* const out = (bf16*)p.out + (long)zb * p.s * p.h + zh * HD;
+  if (t)
+    store_rows_lds(st.o, t, out, p.h, q0, p.s, lane, inv);
+  else
+    store_dT(st.o, out, p.h, qq, p.s, lane, inv);
   if (lane < 32 && qq < p.s) p.lse[(long)z * p.s + qq] = st.m_run + __builtin_amdgcn_logf(l_tot);
 }
 
@@ -385,7 +420,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     stage_sync();
   }
   if (kb < nkb) compute(lds0, kb);
-  fwd_store(st, p, z, qq, lane);
+  __syncthreads();  // every wave is done with the tiles: lds0 holds the output rows
+  fwd_store(st, p, z, q0, qq, lane, lds0 + wave * 32 * ROWB);
 }
 
 // Causal forward over pairs of query blocks.  Query block q needs the key
@@ -458,7 +494,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   auto step = [&](int it, const char* cur, char* nxt) {
     const int j = j0 + it;
     if (it < cnt && j == na && qcur != qb) {  // group 0 leaves qa: its rows are complete
-      fwd_store(st, p, z, qq, lane);
+      fwd_store(st, p, z, q0, qq, lane);
       st.reset();
       qcur = qb;
       q0 = qcur * 128 + 32 * wg;
@@ -489,7 +525,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // conflict-free), group 1 combines it with its own and stores.
   if (grp == 0) {
     if (qcur != qb) {  // no step of qb in this half: qa is complete, qb's share is empty
-      fwd_store(st, p, z, qq, lane);
+      fwd_store(st, p, z, q0, qq, lane, lds + FWD_GROUP + 4 * 32 * ROWB + wg * 32 * ROWB);
       st.reset();
     }
     float4* dst = (float4*)lds + wg * 16 * 64 + lane;
@@ -519,7 +555,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
     st.l_run = ml.y * a0 + st.l_run * a1;
     st.m_run = m;
-    fwd_store(st, p, z, qq, lane);
+    fwd_store(st, p, z, q0, qq, lane, lds + FWD_GROUP + wg * 32 * ROWB);
   }
 }
 
@@ -632,10 +668,11 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_k(AttnArgs p) {
     stage_sync();
   }
   if (i < n) compute(lds0, qb0 + i);
+  __syncthreads();  // every wave is done with the tiles: lds0 holds the output rows
 
   bf16* dK = p.out + (long)zb * p.s * ld + p.h + zh * HD;
-  store_dT(dk, dK, ld, key, p.s, lane, p.scale);
-  store_dT(dv, dK + p.h, ld, key, p.s, lane, 1.0f);
+  store_rows_lds(dk, lds0 + wave * 32 * ROWB, dK, ld, k0w, p.s, lane, p.scale);
+  store_rows_lds(dv, lds0 + wave * 32 * ROWB, dK + p.h, ld, k0w, p.s, lane, 1.0f);
 }
 
 // Backward over query blocks: dQ.  Per wave: 32 queries (Q and dO rows
@@ -706,11 +743,17 @@ __device__ __forceinline__ void bwdq_block(f32x16 (&dq)[HD / 32], const BwdQRows
   }
 }
 
-__device__ __forceinline__ void store_dq(const f32x16 (&dq)[HD / 32], const AttnArgs& p, int z, int qq,
-                                         int lane) {
+// dQ rows q0..q0+31 of the wave (this lane's qq); through LDS area t (8 KB)
+// when given.
+__device__ __forceinline__ void store_dq(const f32x16 (&dq)[HD / 32], const AttnArgs& p, int z, int q0,
+                                         int qq, int lane, char* t = nullptr) {
   const int zb = z / p.heads, zh = z % p.heads;
   const long ld = 3L * p.h;
-  store_dT(dq, p.out + (long)zb * p.s * ld + zh * HD, ld, qq, p.s, lane, p.scale);
+  bf16* const out = p.out + (long)zb * p.s * ld + zh * HD;
+  if (t)
+    store_rows_lds(dq, t, out, ld, q0, p.s, lane, p.scale);
+  else
+    store_dT(dq, out, ld, qq, p.s, lane, p.scale);
 }
 
 // One query block of 128 per workgroup (4 waves), two stages of K and V.
@@ -764,7 +807,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     stage_sync();
   }
   if (kb < nkb) compute(lds0, kb);
-  store_dq(dq, p, z, qq, lane);
+  __syncthreads();  // every wave is done with the tiles: lds0 holds the output rows
+  store_dq(dq, p, z, q0, qq, lane, lds0 + wave * 32 * ROWB);
 }
 
 // Causal dQ over pairs of query blocks: the work split of attn_fwd_pair_k
@@ -830,7 +874,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   auto step = [&](int it, const char* cur, char* nxt) {
     const int j = j0 + it;
     if (it < cnt && j == na && qcur != qb) {  // group 0 leaves qa: its rows are complete
-      store_dq(dq, p, z, qq, lane);
+      store_dq(dq, p, z, q0, qq, lane);
 #pragma unroll
       for (int b = 0; b < HD / 32; ++b) zero(dq[b]);
       qcur = qb;
@@ -866,7 +910,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 
   if (grp == 0) {
     if (qcur != qb) {  // no step of qb in this half: qa is complete, qb's share is zero
-      store_dq(dq, p, z, qq, lane);
+      store_dq(dq, p, z, q0, qq, lane, lds + FWD_GROUP + 4 * 32 * ROWB + wg * 32 * ROWB);
 #pragma unroll
       for (int b = 0; b < HD / 32; ++b) zero(dq[b]);
     }
@@ -890,7 +934,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         dq[b][4 * c + 2] = v.z + dq[b][4 * c + 2];
         dq[b][4 * c + 3] = v.w + dq[b][4 * c + 3];
       }
-    store_dq(dq, p, z, qq, lane);
+    store_dq(dq, p, z, q0, qq, lane, lds + FWD_GROUP + wg * 32 * ROWB);
   }
 }
 
