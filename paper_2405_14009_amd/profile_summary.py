@@ -59,7 +59,7 @@ def kernel_class(name: str) -> str:
         return "gemm_other"
     if "gemm_f32" in name:
         return "gemm_f32"
-    if "attn_fwd_k" in name:
+    if re.search(r"attn_fwd(_pair)?_k", name):
         return "attn_fwd"
     if "attn_bwd" in name:
         return "attn_bwd"
