@@ -286,10 +286,13 @@ enum {
   RC_K_GEMM_WGRAD = 2,  /* weight-gradient linear GEMMs (B_weight) */
   RC_K_ATTN_FWD = 3,    /* attention core forward (one region per layer) */
   RC_K_ATTN_BWD = 4,    /* attention core backward (one region per layer) */
-  RC_K_LN = 5,          /* LayerNorm forward / input-gradient kernels */
+  RC_K_LN = 5,          /* LayerNorm forward / input-gradient kernels; the first layer's forward
+                           also copies the stage input into the stash, the last layer's LN2
+                           backward the upstream gradient */
   RC_K_REDUCE = 6,      /* bias and LayerNorm-affine gradient reductions */
   RC_K_ADAM = 7,        /* fused AdamW */
-  RC_K_COPY = 8,        /* stage input / upstream gradient copied into the stash */
+  RC_K_COPY = 8,        /* separate device copies (none at present: the stash copies of the
+                           stage input and upstream gradient ride on the LayerNorm kernels) */
   RC_K_COUNT = 9
 };
 

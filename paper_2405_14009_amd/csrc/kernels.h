@@ -5,15 +5,17 @@
 #include <hip/hip_runtime.h>
 
 // LayerNorm forward over rows of width h: y = (x - mean) * rstd * g + b;
-// mean and rstd (fp32) are saved per row.  elt: 2 = bf16, 4 = fp32.
+// mean and rstd (fp32) are saved per row.  elt: 2 = bf16, 4 = fp32.  When
+// xcopy is given, x is also copied there (rows x h elements).
 hipError_t ln_forward(int elt, const void* x, const float* g, const float* b, void* y, float* mean,
-                      float* rstd, long rows, int h, float eps, hipStream_t s);
+                      float* rstd, long rows, int h, float eps, hipStream_t s, void* xcopy = nullptr);
 
 // LayerNorm input gradient plus residual: dx = resid + rstd * (dz - mean(dz)
 // - xhat * mean(dz * xhat)), dz = dout * g, xhat recomputed from x, mean, rstd.
+// When rcopy is given, resid is also copied there (rows x h elements).
 hipError_t ln_backward(int elt, const void* dout, const void* x, const float* mean,
                        const float* rstd, const float* g, const void* resid, void* dx, long rows,
-                       int h, hipStream_t s);
+                       int h, hipStream_t s, void* rcopy = nullptr);
 
 // Column reductions over the rows of nseg segments (one per micro-batch) of
 // a [rows, n] matrix with leading dimension ld, into fp32 outputs (overwrite

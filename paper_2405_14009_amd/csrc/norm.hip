@@ -173,8 +173,8 @@ __device__ __forceinline__ uint4 pack(const float (&f)[4], const float*) {
 template <class E, int MAXC>
 __global__ __launch_bounds__(NT) void ln_fwd_wave_k(const E* __restrict__ x, const float* __restrict__ g,
                                                     const float* __restrict__ b, E* __restrict__ y,
-                                                    float* __restrict__ mean, float* __restrict__ rstd,
-                                                    long rows, int h, float eps) {
+                                                    E* __restrict__ xcopy, float* __restrict__ mean,
+                                                    float* __restrict__ rstd, long rows, int h, float eps) {
   constexpr int EPC = Chunk<E>::N;
   const long row = blockIdx.x * (long)(NT / 64) + (threadIdx.x >> 6);
   if (row >= rows) return;
@@ -236,6 +236,7 @@ __global__ __launch_bounds__(NT) void ln_fwd_wave_k(const E* __restrict__ x, con
 #pragma unroll
       for (int e = 0; e < EPC; ++e) f[e] = (f[e] - mu) * rs * gg[qi][e] + bb[qi][e];
       *(uint4*)(yr + (long)c * EPC) = pack(f, (const E*)nullptr);
+      if (xcopy) *(uint4*)(xcopy + row * h + (long)c * EPC) = v[q];  // the input row, unchanged
     }
   }
   if (lane == 0) {
@@ -250,7 +251,7 @@ __global__ __launch_bounds__(NT) void ln_bwd_wave_k(const E* __restrict__ dout, 
                                                     const float* __restrict__ rstd,
                                                     const float* __restrict__ g,
                                                     const E* __restrict__ resid, E* __restrict__ dx,
-                                                    long rows, int h) {
+                                                    E* __restrict__ rcopy, long rows, int h) {
   constexpr int EPC = Chunk<E>::N;
   const long row = blockIdx.x * (long)(NT / 64) + (threadIdx.x >> 6);
   if (row >= rows) return;
@@ -305,12 +306,15 @@ __global__ __launch_bounds__(NT) void ln_bwd_wave_k(const E* __restrict__ dout, 
       unpack(dv[q], (const E*)nullptr, d);
       unpack(xv[q], (const E*)nullptr, xx);
       const int qi = PRE ? q : 0;
+      uint4 rq;
       if constexpr (PRE) {
-        unpack(rv[q], (const E*)nullptr, r);
+        rq = rv[q];
       } else {
-        unpack(*(const uint4*)(resid + row * h + (long)c * EPC), (const E*)nullptr, r);
+        rq = *(const uint4*)(resid + row * h + (long)c * EPC);
         ld_g(c, gg[0]);
       }
+      unpack(rq, (const E*)nullptr, r);
+      if (rcopy) *(uint4*)(rcopy + row * h + (long)c * EPC) = rq;  // the residual row, unchanged
 #pragma unroll
       for (int e = 0; e < EPC; ++e) {
         const float xh = (xx[e] - mu) * rs;
@@ -374,16 +378,17 @@ __global__ __launch_bounds__(NT) void colsum_part16_k(ColSegs sg, long ld, long 
 }
 
 template <class E, int MAXC>
-void launch_ln_fwd(const void* x, const float* g, const float* b, void* y, float* mean, float* rstd,
-                   long rows, int h, float eps, hipStream_t s) {
+void launch_ln_fwd(const void* x, const float* g, const float* b, void* y, void* xcopy, float* mean,
+                   float* rstd, long rows, int h, float eps, hipStream_t s) {
   hipLaunchKernelGGL((ln_fwd_wave_k<E, MAXC>), dim3((unsigned)((rows + 3) / 4)), dim3(NT), 0, s,
-                     (const E*)x, g, b, (E*)y, mean, rstd, rows, h, eps);
+                     (const E*)x, g, b, (E*)y, (E*)xcopy, mean, rstd, rows, h, eps);
 }
 template <class E, int MAXC>
 void launch_ln_bwd(const void* dout, const void* x, const float* mean, const float* rstd, const float* g,
-                   const void* resid, void* dx, long rows, int h, hipStream_t s) {
+                   const void* resid, void* dx, void* rcopy, long rows, int h, hipStream_t s) {
   hipLaunchKernelGGL((ln_bwd_wave_k<E, MAXC>), dim3((unsigned)((rows + 3) / 4)), dim3(NT), 0, s,
-                     (const E*)dout, (const E*)x, mean, rstd, g, (const E*)resid, (E*)dx, rows, h);
+                     (const E*)dout, (const E*)x, mean, rstd, g, (const E*)resid, (E*)dx, (E*)rcopy, rows,
+                     h);
 }
 
 // chunks per lane of a row of h elements of type E, or 0 when the wave
@@ -398,20 +403,24 @@ int wave_chunks(int elt, int h) {
 }  // namespace
 
 hipError_t ln_forward(int elt, const void* x, const float* g, const float* b, void* y, float* mean,
-                      float* rstd, long rows, int h, float eps, hipStream_t s) {
+                      float* rstd, long rows, int h, float eps, hipStream_t s, void* xcopy) {
   if (rows <= 0) return hipSuccess;
   if (const int per = wave_chunks(elt, h)) {
     if (elt == 2) {
-      if (per <= 4) launch_ln_fwd<bf16, 4>(x, g, b, y, mean, rstd, rows, h, eps, s);
-      else if (per <= 8) launch_ln_fwd<bf16, 8>(x, g, b, y, mean, rstd, rows, h, eps, s);
-      else if (per <= 12) launch_ln_fwd<bf16, 12>(x, g, b, y, mean, rstd, rows, h, eps, s);
-      else launch_ln_fwd<bf16, 24>(x, g, b, y, mean, rstd, rows, h, eps, s);
+      if (per <= 4) launch_ln_fwd<bf16, 4>(x, g, b, y, xcopy, mean, rstd, rows, h, eps, s);
+      else if (per <= 8) launch_ln_fwd<bf16, 8>(x, g, b, y, xcopy, mean, rstd, rows, h, eps, s);
+      else if (per <= 12) launch_ln_fwd<bf16, 12>(x, g, b, y, xcopy, mean, rstd, rows, h, eps, s);
+      else launch_ln_fwd<bf16, 24>(x, g, b, y, xcopy, mean, rstd, rows, h, eps, s);
     } else {
-      if (per <= 4) launch_ln_fwd<float, 4>(x, g, b, y, mean, rstd, rows, h, eps, s);
-      else if (per <= 8) launch_ln_fwd<float, 8>(x, g, b, y, mean, rstd, rows, h, eps, s);
-      else launch_ln_fwd<float, 24>(x, g, b, y, mean, rstd, rows, h, eps, s);
+      if (per <= 4) launch_ln_fwd<float, 4>(x, g, b, y, xcopy, mean, rstd, rows, h, eps, s);
+      else if (per <= 8) launch_ln_fwd<float, 8>(x, g, b, y, xcopy, mean, rstd, rows, h, eps, s);
+      else launch_ln_fwd<float, 24>(x, g, b, y, xcopy, mean, rstd, rows, h, eps, s);
     }
     return hipGetLastError();
+  }
+  if (xcopy) {  // the row-per-workgroup kernel writes y only
+    const hipError_t e = hipMemcpyAsync(xcopy, x, (size_t)rows * h * elt, hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return e;
   }
   if (elt == 2)
     hipLaunchKernelGGL(ln_fwd_k<bf16>, dim3(rows), dim3(NT), 0, s, (const bf16*)x, g, b, (bf16*)y,
@@ -424,20 +433,24 @@ hipError_t ln_forward(int elt, const void* x, const float* g, const float* b, vo
 
 hipError_t ln_backward(int elt, const void* dout, const void* x, const float* mean,
                        const float* rstd, const float* g, const void* resid, void* dx, long rows,
-                       int h, hipStream_t s) {
+                       int h, hipStream_t s, void* rcopy) {
   if (rows <= 0) return hipSuccess;
   if (const int per = wave_chunks(elt, h)) {
     if (elt == 2) {
-      if (per <= 4) launch_ln_bwd<bf16, 4>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
-      else if (per <= 8) launch_ln_bwd<bf16, 8>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
-      else if (per <= 12) launch_ln_bwd<bf16, 12>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
-      else launch_ln_bwd<bf16, 24>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
+      if (per <= 4) launch_ln_bwd<bf16, 4>(dout, x, mean, rstd, g, resid, dx, rcopy, rows, h, s);
+      else if (per <= 8) launch_ln_bwd<bf16, 8>(dout, x, mean, rstd, g, resid, dx, rcopy, rows, h, s);
+      else if (per <= 12) launch_ln_bwd<bf16, 12>(dout, x, mean, rstd, g, resid, dx, rcopy, rows, h, s);
+      else launch_ln_bwd<bf16, 24>(dout, x, mean, rstd, g, resid, dx, rcopy, rows, h, s);
     } else {
-      if (per <= 4) launch_ln_bwd<float, 4>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
-      else if (per <= 8) launch_ln_bwd<float, 8>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
-      else launch_ln_bwd<float, 24>(dout, x, mean, rstd, g, resid, dx, rows, h, s);
+      if (per <= 4) launch_ln_bwd<float, 4>(dout, x, mean, rstd, g, resid, dx, rcopy, rows, h, s);
+      else if (per <= 8) launch_ln_bwd<float, 8>(dout, x, mean, rstd, g, resid, dx, rcopy, rows, h, s);
+      else launch_ln_bwd<float, 24>(dout, x, mean, rstd, g, resid, dx, rcopy, rows, h, s);
     }
     return hipGetLastError();
+  }
+  if (rcopy) {  // the row-per-workgroup kernel writes dx only
+    const hipError_t e = hipMemcpyAsync(rcopy, resid, (size_t)rows * h * elt, hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return e;
   }
   if (elt == 2)
     hipLaunchKernelGGL(ln_bwd_k<bf16>, dim3(rows), dim3(NT), 0, s, (const bf16*)dout, (const bf16*)x,

@@ -418,19 +418,16 @@ rc_status run_forward(rc_stage* st, int ws, int fs, const void* x, void* yout) {
   const int E = y.elt, L = y.L;
   const long T = y.T, h = y.h, f = y.f;
   hipStream_t s = st->stream;
-  {
-    Prof pr(st, RC_K_COPY, 0, 2.0 * T * h * E);
-    HIPCHK(hipMemcpyAsync(wptr(st, ws, 0).X, x, T * h * E, hipMemcpyDeviceToDevice, s));
-  }
   const double ln_f_bytes = 2.0 * T * h * E + 8.0 * T + 8.0 * h;
   const double att = (y.causal ? 1.0 : 2.0) * y.b * (double)y.s * y.s * h;
   for (int l = 0; l < L; ++l) {
     WPtr w = wptr(st, ws, l);
     FPtr fl = fptr(st, fs, l);
     {
-      Prof pr1(st, RC_K_LN, 0, ln_f_bytes);
-      HIPCHK(ln_forward(E, w.X, master(st, l, RC_P_LN1_G), master(st, l, RC_P_LN1_B), w.A, w.mu1,
-                        w.r1, T, y.h, y.eps, s));
+      // layer 0 reads the caller's x and also copies it into the stash
+      Prof pr1(st, RC_K_LN, 0, ln_f_bytes + (l == 0 ? (double)T * h * E : 0.0));
+      HIPCHK(ln_forward(E, l == 0 ? x : w.X, master(st, l, RC_P_LN1_G), master(st, l, RC_P_LN1_B), w.A,
+                        w.mu1, w.r1, T, y.h, y.eps, s, l == 0 ? w.X : nullptr));
     }
     GemmParams g = gp(T, 3 * h, h, w.A, h, 1, weight(st, l, RC_P_W_QKV), 3 * h, 0, EPI_BIAS, fl.QKV, 3 * h);
     g.bias = master(st, l, RC_P_B_QKV);
@@ -471,17 +468,17 @@ rc_status run_backward_input(rc_stage* st, int ws, int fs, const void* dy, void*
   const long T = y.T, h = y.h, f = y.f;
   hipStream_t s = st->stream;
   char* dO = st->work + y.off_dO;
-  {
-    Prof pr(st, RC_K_COPY, 0, 2.0 * T * h * E);
-    HIPCHK(hipMemcpyAsync(wptr(st, ws, L - 1).dY, dy, T * h * E, hipMemcpyDeviceToDevice, s));
-  }
   const double ln_b_bytes = 4.0 * T * h * E + 8.0 * T + 4.0 * h;
   const double att = (y.causal ? 1.0 : 2.0) * y.b * (double)y.s * y.s * h;
   for (int l = L - 1; l >= 0; --l) {
     WPtr w = wptr(st, ws, l);
     FPtr fl = fptr(st, fs, l);
+    // The last layer reads the caller's dy; its LN2 backward, which adds dy as
+    // the residual, also copies it into the stash for the weight pass.
+    const bool top = l == L - 1;
+    char* const dYl = top ? (char*)dy : w.dY;
     // dU = (dY W_2^T) * gelu'(U)
-    GemmParams g = gp(T, f, h, w.dY, h, 1, weight(st, l, RC_P_W_2), h, 1, EPI_GELU_BWD, w.dU, f);
+    GemmParams g = gp(T, f, h, dYl, h, 1, weight(st, l, RC_P_W_2), h, 1, EPI_GELU_BWD, w.dU, f);
     g.aux = fl.U;
     g.ld_aux = f;
     HIPCHK(gemm_lin(st, g, RC_K_GEMM_DGRAD));
@@ -490,8 +487,9 @@ rc_status run_backward_input(rc_stage* st, int ws, int fs, const void* dy, void*
     HIPCHK(gemm_lin(st, g, RC_K_GEMM_DGRAD));
     // dH = dY + LN2^T(dC)
     {
-      Prof pr(st, RC_K_LN, 0, ln_b_bytes);
-      HIPCHK(ln_backward(E, w.dC, w.H, w.mu2, w.r2, master(st, l, RC_P_LN2_G), w.dY, w.dH, T, y.h, s));
+      Prof pr(st, RC_K_LN, 0, ln_b_bytes + (top ? (double)T * h * E : 0.0));
+      HIPCHK(ln_backward(E, w.dC, w.H, w.mu2, w.r2, master(st, l, RC_P_LN2_G), dYl, w.dH, T, y.h, s,
+                         top ? w.dY : nullptr));
     }
     // dO = dH W_o^T
     g = gp(T, h, h, w.dH, h, 1, weight(st, l, RC_P_W_O), h, 1, EPI_STORE, dO, h);
