@@ -440,8 +440,13 @@ constexpr int FWD_STAGE = 2 * TILE64;        // K | V of one key block
 constexpr int FWD_GROUP = 2 * FWD_STAGE;     // two stages per wave group
 
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_pair_k(AttnArgs p) {
-  __shared__ __attribute__((aligned(1024))) char lds[2 * FWD_GROUP + 1024];
+  // [group 0 stages | group 1 stages | L2-warming sink | merge statistics];
+  // after the loop the stages hold group 0's partial O (first 64 KB) and the
+  // output rows on their way to memory (the next 64 KB), so the statistics
+  // the merge reads have an area of their own
+  __shared__ __attribute__((aligned(1024))) char lds[2 * FWD_GROUP + 1024 + 2048];
   char* const sink = lds + 2 * FWD_GROUP;
+  float2* const mstat = (float2*)(lds + 2 * FWD_GROUP + 1024);  // qb's (maximum, sum) per [wave][lane]
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int grp = wave >> 2, wg = wave & 3;
@@ -535,11 +540,11 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       for (int c = 0; c < 4; ++c)
         dst[(4 * b + c) * 64] = make_float4(st.o[b][4 * c], st.o[b][4 * c + 1], st.o[b][4 * c + 2],
                                             st.o[b][4 * c + 3]);
-    ((float2*)(lds + FWD_GROUP))[wg * 64 + lane] = make_float2(st.m_run, st.l_run);
+    mstat[wg * 64 + lane] = make_float2(st.m_run, st.l_run);
   }
   __syncthreads();
   if (grp == 1) {
-    const float2 ml = ((const float2*)(lds + FWD_GROUP))[wg * 64 + lane];
+    const float2 ml = mstat[wg * 64 + lane];
     const float m = fmaxf(ml.x, st.m_run);
     const float a0 = __builtin_amdgcn_exp2f(ml.x - m), a1 = __builtin_amdgcn_exp2f(st.m_run - m);
     const float4* src = (const float4*)lds + wg * 16 * 64 + lane;
