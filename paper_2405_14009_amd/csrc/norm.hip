@@ -105,31 +105,39 @@ __global__ __launch_bounds__(NT) void colsum_part_k(ColSegs sg, long ld, long ro
 }
 
 // Middle stage of the column sums: block row g sums partial rows
-// [32 g, 32 g + 32) in order (a fixed tree: partials -> groups of 32 -> final).
-constexpr int MID = 32;
+// [MID g, MID g + MID) in order (a fixed tree: partials -> groups of MID ->
+// final); blockIdx.z selects the array (0: the plain sums, 1: the LN-gamma
+// sums, stored right after them, as are their groups).
+constexpr int MID = 16;
 __global__ __launch_bounds__(NT) void colsum_mid_k(const float* __restrict__ part, int nchunk, int n,
                                                    float* __restrict__ mid) {
   const int c = 4 * (blockIdx.x * NT + threadIdx.x);
   if (c >= n) return;
+  const float* src = part + (long)blockIdx.z * nchunk * n;
+  float* dst = mid + (long)blockIdx.z * gridDim.y * n;
   const int r0 = blockIdx.y * MID, r1 = min(nchunk, r0 + MID);
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int r = r0; r < r1; ++r) {
-    const float4 v = *(const float4*)(part + (long)r * n + c);
+    const float4 v = *(const float4*)(src + (long)r * n + c);
     s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
   }
-  *(float4*)(mid + (long)blockIdx.y * n + c) = s;
+  *(float4*)(dst + (long)blockIdx.y * n + c) = s;
 }
 
-__global__ __launch_bounds__(NT) void colsum_final_k(const float* __restrict__ part, int nchunk,
-                                                     int n, float* __restrict__ out, int accumulate) {
+// Last stage: rows [0, nchunk) into out_b (blockIdx.y = 0) or rows
+// [nchunk, 2 nchunk) into out_g (blockIdx.y = 1), in order.
+__global__ __launch_bounds__(NT) void colsum_final_k(const float* __restrict__ part, int nchunk, int n,
+                                                     float* __restrict__ out_b, float* __restrict__ out_g,
+                                                     int accumulate) {
   const int c = 4 * (blockIdx.x * NT + threadIdx.x);
   if (c >= n) return;
+  const float* src = part + (long)blockIdx.y * nchunk * n;
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int ch = 0; ch < nchunk; ++ch) {
-    const float4 v = *(const float4*)(part + (long)ch * n + c);
+    const float4 v = *(const float4*)(src + (long)ch * n + c);
     s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
   }
-  float4* o = (float4*)(out + c);
+  float4* o = (float4*)((blockIdx.y ? out_g : out_b) + c);
   if (accumulate) {
     const float4 v = *o;
     s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
@@ -503,21 +511,18 @@ hipError_t colsum(int elt, bool ln, const ColSegs& sg, int nseg, long ld, long r
         hipLaunchKernelGGL((colsum_part_k<float, false>), grid, dim3(NT), 0, s, sg, ld, rows, n, cps, part_b, part_g);
     }
   }
-  // partial rows -> groups of MID (wide grid) -> one row per column
-  const float* fin_b = part_b;
-  const float* fin_g = part_g;
+  // partial rows -> groups of MID (wide grid) -> one row per column; the plain
+  // and (LN) gamma arrays share each launch
+  const int narr = ln ? 2 : 1;
+  const float* fin = part_b;  // the gamma rows follow the plain ones at every stage
   int nfin = nchunk;
   if (nchunk > MID) {
     const int ng = (nchunk + MID - 1) / MID;
-    float* mid_b = part + 2L * nchunk * n;
-    float* mid_g = mid_b + (long)ng * n;
-    hipLaunchKernelGGL(colsum_mid_k, dim3(cb, ng), dim3(NT), 0, s, (const float*)part_b, nchunk, n, mid_b);
-    if (ln) hipLaunchKernelGGL(colsum_mid_k, dim3(cb, ng), dim3(NT), 0, s, (const float*)part_g, nchunk, n, mid_g);
-    fin_b = mid_b;
-    fin_g = mid_g;
+    float* mid = part + 2L * nchunk * n;
+    hipLaunchKernelGGL(colsum_mid_k, dim3(cb, ng, narr), dim3(NT), 0, s, (const float*)part_b, nchunk, n, mid);
+    fin = mid;
     nfin = ng;
   }
-  hipLaunchKernelGGL(colsum_final_k, dim3(cb), dim3(NT), 0, s, fin_b, nfin, n, db, accumulate);
-  if (ln) hipLaunchKernelGGL(colsum_final_k, dim3(cb), dim3(NT), 0, s, fin_g, nfin, n, dg, accumulate);
+  hipLaunchKernelGGL(colsum_final_k, dim3(cb, narr), dim3(NT), 0, s, fin, nfin, n, db, dg, accumulate);
   return hipGetLastError();
 }
