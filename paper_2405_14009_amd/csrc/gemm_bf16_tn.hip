@@ -5,13 +5,23 @@
 
 namespace {
 
-// out[n] (+)= sum over the rows r of work[r][n], in row order.
+// out[n] (+)= sum over the rows r of work[r][n], in row order.  Rows are
+// requested 16 at a time and then added in order (one load in flight per
+// thread made the 64-row sums of a 16384-row product take 30 us).
 __global__ __launch_bounds__(256) void colsum_rows_k(const float* __restrict__ work, int rows, int n,
                                                      float* __restrict__ out, int accumulate) {
   const int c = blockIdx.x * 256 + threadIdx.x;
   if (c >= n) return;
   float t = 0.f;
-  for (int r = 0; r < rows; ++r) t += work[(long)r * n + c];
+  int r = 0;
+  for (; r + 16 <= rows; r += 16) {
+    float v[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = work[(long)(r + i) * n + c];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) t += v[i];
+  }
+  for (; r < rows; ++r) t += work[(long)r * n + c];
   out[c] = (accumulate ? out[c] : 0.f) + t;
 }
 

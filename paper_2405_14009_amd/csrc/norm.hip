@@ -104,6 +104,28 @@ __global__ __launch_bounds__(NT) void colsum_part_k(ColSegs sg, long ld, long ro
   if (LN) *(float4*)(part_g + (long)blockIdx.y * n + c) = sgm;
 }
 
+// Sum of rows [r0, r1) of columns c..c+3 of a [rows][n] fp32 array, in row
+// order; rows are requested 8 at a time before they are added, so the loads
+// overlap instead of each waiting for the previous sum.
+__device__ __forceinline__ float4 sum_rows4(const float* src, int r0, int r1, int n, int c) {
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  int r = r0;
+  for (; r + 8 <= r1; r += 8) {
+    float4 v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = *(const float4*)(src + (long)(r + i) * n + c);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      s.x += v[i].x; s.y += v[i].y; s.z += v[i].z; s.w += v[i].w;
+    }
+  }
+  for (; r < r1; ++r) {
+    const float4 v = *(const float4*)(src + (long)r * n + c);
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  return s;
+}
+
 // Middle stage of the column sums: block row g sums partial rows
 // [MID g, MID g + MID) in order (a fixed tree: partials -> groups of MID ->
 // final); blockIdx.z selects the array (0: the plain sums, 1: the LN-gamma
@@ -116,12 +138,7 @@ __global__ __launch_bounds__(NT) void colsum_mid_k(const float* __restrict__ par
   const float* src = part + (long)blockIdx.z * nchunk * n;
   float* dst = mid + (long)blockIdx.z * gridDim.y * n;
   const int r0 = blockIdx.y * MID, r1 = min(nchunk, r0 + MID);
-  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int r = r0; r < r1; ++r) {
-    const float4 v = *(const float4*)(src + (long)r * n + c);
-    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-  }
-  *(float4*)(dst + (long)blockIdx.y * n + c) = s;
+  *(float4*)(dst + (long)blockIdx.y * n + c) = sum_rows4(src, r0, r1, n, c);
 }
 
 // Last stage: rows [0, nchunk) into out_b (blockIdx.y = 0) or rows
@@ -132,11 +149,7 @@ __global__ __launch_bounds__(NT) void colsum_final_k(const float* __restrict__ p
   const int c = 4 * (blockIdx.x * NT + threadIdx.x);
   if (c >= n) return;
   const float* src = part + (long)blockIdx.y * nchunk * n;
-  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int ch = 0; ch < nchunk; ++ch) {
-    const float4 v = *(const float4*)(src + (long)ch * n + c);
-    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-  }
+  float4 s = sum_rows4(src, 0, nchunk, n, c);
   float4* o = (float4*)((blockIdx.y ? out_g : out_b) + c);
   if (accumulate) {
     const float4 v = *o;
