@@ -181,7 +181,7 @@ def main() -> int:
             if events is not None:
                 b = torch.cuda.Event(enable_timing=True)
                 b.record()
-                events.append((kind, a, b))
+                events.append((kind, a, b, len(mbs)))
 
     for i in range(args.warmup):
         run_step()
@@ -239,11 +239,17 @@ def main() -> int:
     }
     if profile:
         per = {"F": 0.0, "B": 0.0, "W": 0.0, "STEP": 0.0}
-        for kind, a, b in events:
-            per[kind] += a.elapsed_time(b)
+        calls = {"F": [], "B": [], "W": []}  # TFLOP/s of each call (a W call may cover several micro-batches)
+        pass_fl = {"F": F, "B": B, "W": W}
+        for kind, a, b, nmb in events:
+            ms = a.elapsed_time(b)
+            per[kind] += ms
+            if kind in calls and ms > 0:
+                calls[kind].append(cfg.layers * nmb * pass_fl[kind] / (ms / 1e3) / 1e12)
         nl = cfg.layers * cfg.n_mb * args.steps
         out["pass_tflops"] = {k: round(nl * fl / (per[k] / 1e3) / 1e12, 2)
                               for k, fl in (("F", F), ("B", B), ("W", W))}
+        out["pass_tflops_median"] = {k: round(float(np.median(v)), 2) for k, v in calls.items() if v}
         out["pass_ms_per_mb"] = {k: round(per[k] / (cfg.n_mb * args.steps), 3) for k in ("F", "B", "W")}
         out["optimizer_ms"] = round(per["STEP"] / args.steps, 3)
         prof = stage.profile_read()
