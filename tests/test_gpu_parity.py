@@ -104,6 +104,8 @@ def test_elementwise_parity(name):
     dict(seq=328, causal=False, micro_batch=3, n_mb=2),
     dict(seq=64, micro_batch=3, n_mb=2),              # one key block
     dict(seq=1000, n_mb=2),                           # 8 query blocks: 4 pairs of unequal halves
+    dict(seq=136, n_mb=2),                            # 2 query blocks, the last one's key range capped at s
+    dict(seq=8, micro_batch=4, n_mb=2),               # the shortest sequence the stage takes
 ])
 def test_attention_variants_parity(variant):
     """bf16 stages with head dimension 128 take the fused attention path
