@@ -112,8 +112,8 @@ def main() -> int:
                     help="skip the per-kernel events (for external profilers)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one stage on one GPU; runs on more than one GPU are not part of "
-              "this build (use --gpus 1)", file=sys.stderr)
+        print("bench.py measures one stage on one GPU; the library runs no collectives, so there "
+              "is no multi-GPU run to measure (use --gpus 1)", file=sys.stderr)
         return 2
 
     import numpy as np

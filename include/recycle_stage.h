@@ -54,7 +54,7 @@ typedef enum rc_status {
   RC_ERR_BAD_STATE = -2,     /* call out of order for this micro-batch / iteration */
   RC_ERR_OUT_OF_STASH = -3,  /* no free stash slot for another forward */
   RC_ERR_HIP = -4,           /* a HIP runtime call or kernel launch failed */
-  RC_ERR_UNSUPPORTED = -5    /* shape or option this build does not implement */
+  RC_ERR_UNSUPPORTED = -5    /* shape or option the library does not implement */
 } rc_status;
 
 typedef enum rc_dtype {
