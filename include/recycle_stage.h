@@ -62,9 +62,15 @@ typedef enum rc_dtype {
   RC_BF16 = 1   /* bf16 activations / weight copies, fp32 accumulation, fp32 grads, master weights and Adam moments */
 } rc_dtype;
 
-/* Shape of the stage.  Requirements: hidden % heads == 0; hidden, ffn,
- * seq_len and head_dim = hidden/heads are multiples of 8 (otherwise
- * RC_ERR_UNSUPPORTED).  causal = 1 masks keys after the query (GPT). */
+/* Shape of the stage.  Requirements (otherwise RC_ERR_UNSUPPORTED):
+ *  - hidden % heads == 0; hidden, ffn, seq_len and head_dim = hidden/heads
+ *    are multiples of 8;
+ *  - bf16 stages: every matrix the matrix-core kernels read through a
+ *    buffer descriptor fits its 2^31 - 1 byte range: 2 T max(3 hidden, ffn)
+ *    (activation operands, T = micro_batch * seq_len), 2 hidden
+ *    max(3 hidden, ffn) (weights) and, without fused attention, 2 seq_len^2
+ *    (one head's probabilities).
+ * causal = 1 masks keys after the query (GPT). */
 typedef struct rc_stage_config {
   int32_t num_layers;
   int32_t hidden;
@@ -189,9 +195,10 @@ rc_status rc_stage_backward(rc_stage* st, rc_mb mb, const void* dy, void* dx);
  * Errors: RC_ERR_BAD_STATE (mb has not run B, or already ran W), RC_ERR_HIP. */
 rc_status rc_stage_backward_weight(rc_stage* st, rc_mb mb);
 
-/* B_weight of n micro-batches mbs[0..n) at once (the weight pass may be
- * deferred and run in any order and grouping, Sec. 3.2; gradients are sums
- * over micro-batches, Eq. 1).  Same result and op-log records as n
+/* B_weight of n micro-batches mbs[0..n) at once (the weight pass is
+ * dependence-free once its own B_input ran, so it may be deferred and run in
+ * any order and grouping, section 3.2; re-routing leaves the computation, a
+ * sum of per-micro-batch gradients, unchanged, section 3.1).  Same result and op-log records as n
  * consecutive rc_stage_backward_weight calls in the given order (fp32 sums
  * in another association order), but each linear's gradient is one product
  * over the n micro-batches' concatenated tokens and each bias / LayerNorm
@@ -316,6 +323,19 @@ rc_status rc_stage_profile_enable(rc_stage* st, int32_t enable);
 /* Wait for the stream and copy the RC_K_COUNT class profiles into out
  * (out[i].kind == i).  Errors: RC_ERR_INVALID_ARG, RC_ERR_HIP. */
 rc_status rc_stage_profile_read(rc_stage* st, rc_kernel_stat* out);
+
+/* Attention kernels the handle's F and B_input run (chosen from the shape
+ * and the compute-unit count of the current device):
+ *   RC_ATTN_MATERIALISED  scores and probabilities in memory, GEMM + softmax
+ *                         kernels (fp32 stages, head_dim != 128);
+ *   RC_ATTN_BLOCK         fused online softmax, one workgroup per block of
+ *                         128 queries (non-causal, or causal grids that would
+ *                         fill the last round of paired workgroups poorly);
+ *   RC_ATTN_PAIRED        fused causal, one workgroup per pair of query
+ *                         blocks (q, last - q) of equal total length.
+ * Host only; works on dry-run handles.  Errors: RC_ERR_INVALID_ARG. */
+enum { RC_ATTN_MATERIALISED = 0, RC_ATTN_BLOCK = 1, RC_ATTN_PAIRED = 2 };
+rc_status rc_stage_attention_kernels(rc_stage* st, int32_t* kind);
 
 /* Wait for the handle's stream; reports any deferred device error as RC_ERR_HIP. */
 rc_status rc_stage_synchronize(rc_stage* st);

@@ -16,6 +16,7 @@ RC_FP32, RC_BF16 = 0, 1
 RC_OP_F, RC_OP_B, RC_OP_W, RC_OP_STEP, RC_OP_SKIP, RC_OP_ROLLBACK = 0, 1, 2, 3, 4, 5
 RC_READ_PARAM, RC_READ_GRAD, RC_READ_ADAM_M, RC_READ_ADAM_V = 0, 1, 2, 3
 RC_NUM_PARAMS = 12
+RC_ATTN_MATERIALISED, RC_ATTN_BLOCK, RC_ATTN_PAIRED = 0, 1, 2
 
 # Every symbol the header declares, for load checks.
 EXPORTED = (
@@ -24,7 +25,7 @@ EXPORTED = (
     "rc_stage_backward_weight", "rc_stage_stash_account", "rc_stage_set_stash_limit",
     "rc_stage_backward_weight_many", "rc_stage_optimizer_step", "rc_stage_grad_check",
     "rc_stage_optimizer_skip", "rc_stage_optimizer_rollback", "rc_stage_op_log",
-    "rc_stage_stash_usage", "rc_stage_set_stream",
+    "rc_stage_stash_usage", "rc_stage_set_stream", "rc_stage_attention_kernels",
     "rc_stage_synchronize", "rc_stage_profile_enable", "rc_stage_profile_read", "rc_last_error",
     "rc_failure_normalization", "rc_schedule_simulate",
 )
@@ -121,6 +122,7 @@ def load() -> ctypes.CDLL:
         "rc_stage_op_log": [P, ctypes.POINTER(RcOpRecord), I32, ctypes.POINTER(I32)],
         "rc_stage_stash_usage": [P, ctypes.POINTER(I32), ctypes.POINTER(I32)],
         "rc_stage_set_stream": [P, P],
+        "rc_stage_attention_kernels": [P, ctypes.POINTER(I32)],
         "rc_stage_synchronize": [P],
         "rc_stage_profile_enable": [P, I32],
         "rc_stage_profile_read": [P, ctypes.POINTER(RcKernelStat)],

@@ -989,6 +989,11 @@ bool pair_grid_fills(long wgs) {
 
 bool attn_flash_supported(int elt, int head_dim) { return elt == 2 && head_dim == HD; }
 
+bool attn_flash_paired(int b, int s, int heads) {
+  const int nqb = (s + 127) / 128;
+  return pair_grid_fills((long)((nqb + 1) / 2) * b * heads);
+}
+
 hipError_t attn_flash_forward(const void* qkv, void* o, float* lse, int b, int s, int heads, int h,
                               int causal, hipStream_t st) {
   if (h != heads * HD) return hipErrorInvalidValue;

@@ -51,6 +51,10 @@ hipError_t softmax_backward(int elt, const float* dP, const void* P, void* dS, l
 // dV into the three column blocks of dqkv [b*s, 3h]; dv_scratch holds b*heads*s
 // floats.  h == heads * 128.
 bool attn_flash_supported(int elt, int head_dim);
+// Whether causal fused attention over b sequences of s tokens and `heads`
+// heads runs the paired kernels (one workgroup per pair of query blocks) on
+// the current device, rather than one workgroup per query block.
+bool attn_flash_paired(int b, int s, int heads);
 hipError_t attn_flash_forward(const void* qkv, void* o, float* lse, int b, int s, int heads, int h,
                               int causal, hipStream_t st);
 hipError_t attn_flash_backward(const void* qkv, const void* o, const void* dout, const float* lse,

@@ -1,6 +1,7 @@
-// LayerNorm forward / input-gradient kernels (one workgroup per token row,
-// fp32 statistics, wavefront-shuffle reductions) and the deterministic
-// column reductions of the weight pass (bias and LayerNorm-affine gradients).
+// LayerNorm forward / input-gradient kernels (one wave per token row; rows
+// too long for one wave take a workgroup), fp32 statistics, wavefront-shuffle
+// reductions; and the deterministic column reductions of the weight pass
+// (bias and LayerNorm-affine gradients).
 #include "common.h"
 #include "kernels.h"
 

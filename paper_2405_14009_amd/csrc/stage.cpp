@@ -93,6 +93,21 @@ rc_status make_layout(const rc_stage_config* c, Layout& y) {
   const int d = c->hidden / c->heads;
   if (c->hidden % 8 || c->ffn % 8 || c->seq_len % 8 || d % 8)
     return fail(RC_ERR_UNSUPPORTED, "hidden, ffn, seq_len and head_dim must be multiples of 8");
+  if (c->dtype == RC_BF16) {
+    // The matrix-core kernels address their operands through buffer
+    // descriptors whose range is 2^31 - 1 bytes (beyond it a load returns
+    // zeros), so every matrix they read must fit one.
+    const long cap = 0x7fffffffL, wide = std::max(3L * c->hidden, (long)c->ffn);
+    const long T = (long)c->micro_batch * c->seq_len;
+    if (2 * T * wide > cap)
+      return fail(RC_ERR_UNSUPPORTED, "bf16 activation matrix [micro_batch*seq_len, max(3*hidden, ffn)] "
+                                      "exceeds 2^31-1 bytes");
+    if (2L * c->hidden * wide > cap)
+      return fail(RC_ERR_UNSUPPORTED, "bf16 weight matrix [hidden, max(3*hidden, ffn)] exceeds 2^31-1 bytes");
+    if (!attn_flash_supported(2, d) && 2L * c->seq_len * c->seq_len > cap)
+      return fail(RC_ERR_UNSUPPORTED, "bf16 attention probabilities [seq_len, seq_len] of one head "
+                                      "exceed 2^31-1 bytes");
+  }
   y.L = c->num_layers;
   y.h = c->hidden;
   y.a = c->heads;
@@ -1014,6 +1029,14 @@ rc_status rc_stage_stash_usage(rc_stage* st, int32_t* stashed, int32_t* inflight
 rc_status rc_stage_set_stream(rc_stage* st, void* hip_stream) {
   if (!st) return fail(RC_ERR_INVALID_ARG, "null stage");
   st->stream = (hipStream_t)hip_stream;
+  return RC_OK;
+}
+
+rc_status rc_stage_attention_kernels(rc_stage* st, int32_t* kind) {
+  if (!st || !kind) return fail(RC_ERR_INVALID_ARG, "null argument");
+  const Layout& y = st->lay;
+  if (!y.flash) *kind = RC_ATTN_MATERIALISED;
+  else *kind = y.causal && attn_flash_paired(y.b, y.s, y.a) ? RC_ATTN_PAIRED : RC_ATTN_BLOCK;
   return RC_OK;
 }
 

@@ -228,6 +228,14 @@ class Stage:
         L.check(self._lib.rc_stage_stash_usage(self._h, ctypes.byref(a), ctypes.byref(b)))
         return a.value, b.value
 
+    def attention_kernels(self) -> str:
+        """Which attention kernels F and B_input run: "materialised", "block"
+        or "paired" (chosen from the shape and the device's compute units)."""
+        k = ctypes.c_int32()
+        L.check(self._lib.rc_stage_attention_kernels(self._h, ctypes.byref(k)))
+        return {L.RC_ATTN_MATERIALISED: "materialised", L.RC_ATTN_BLOCK: "block",
+                L.RC_ATTN_PAIRED: "paired"}[k.value]
+
     def set_stream(self, stream) -> None:
         self.stream = stream
         L.check(self._lib.rc_stage_set_stream(self._h, ctypes.c_void_p(stream.cuda_stream)))

@@ -112,6 +112,14 @@ TEST_CONFIGS = {
         name="wide_bf16", layers=1, hidden=1152, heads=9, ffn=12288, seq=320, micro_batch=2,
         causal=True, dtype="bf16", n_mb=2, rerouted=(1,), schedule="1f1b_deferred_shuffled_w",
         warmup=2, perturbed=True),
+    # Causal attention whose grid of query-block pairs (4 sequences x 10 heads
+    # x 4 pairs = 160) would fill the last round of 256 compute units poorly,
+    # so F and B_input run the per-query-block kernels, over 8 query blocks of
+    # 128 (key ranges of 2 .. 16 key blocks), as the 40-head 13B stage does.
+    "block_bf16": StageConfig(
+        name="block_bf16", layers=1, hidden=1280, heads=10, ffn=2048, seq=1024, micro_batch=4,
+        causal=True, dtype="bf16", n_mb=2, rerouted=(1,), schedule="1f1b_deferred_shuffled_w",
+        warmup=2, perturbed=True),
     "tiny_noncausal": CONFIGS["tiny"].with_(name="tiny_noncausal", causal=False),
     "tiny_perturbed": CONFIGS["tiny"].with_(name="tiny_perturbed", perturbed=True),
 }

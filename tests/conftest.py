@@ -21,3 +21,21 @@ def rel_l2(a, b) -> float:
     nb = np.linalg.norm(b)
     d = np.linalg.norm(a - b)
     return float(d / nb) if nb > 0 else float(d)
+
+
+def compare_grads(cfg, got, ref, t):
+    """Every gradient of every layer (the K block of the QKV bias, whose exact
+    value is zero, by its norm against the V block's); returns the worst."""
+    h, worst = cfg.hidden, {}
+    for l in range(cfg.layers):
+        for p in range(12):
+            if p == 3:
+                keep = np.r_[0:h, 2 * h:3 * h]
+                worst[(l, p)] = rel_l2(got[l][p][keep], ref[l][p][keep])
+                ratio = np.linalg.norm(got[l][p][h:2 * h]) / np.linalg.norm(got[l][p][2 * h:])
+                assert ratio < t, ("|grad b_k| / |grad b_v|", l, ratio)
+            else:
+                worst[(l, p)] = rel_l2(got[l][p], ref[l][p])
+    bad = {k: v for k, v in worst.items() if v > t}
+    assert not bad, bad
+    return max(worst.values())

@@ -74,6 +74,46 @@ def test_memory_requirements_and_validation():
     assert b"null" in lib.rc_last_error()
 
 
+def test_bf16_configs_beyond_the_descriptor_range_are_refused():
+    """bf16 matrices are read through buffer descriptors of 2^31 - 1 bytes
+    (a load beyond returns zeros), so a configuration with a larger operand
+    is refused up front instead of computing on zeros."""
+    L, lib = lib_or_skip()
+    big = dict(dtype=L.RC_BF16, hidden=4096, heads=32, ffn=16384, seq_len=2048, max_stashed_mb=1,
+               max_inflight_mb=1)
+    # the 6.7B-shaped stage is accepted: 2 * 2048 * 16384 bytes per activation matrix
+    assert _req(_cfg(**big, micro_batch=1))[0] == L.RC_OK
+    # T * max(3h, f) * 2 bytes = 2^31 exactly (one past the range) is refused ...
+    st = _req(_cfg(**big, micro_batch=32))[0]
+    assert st == L.RC_ERR_UNSUPPORTED and b"activation" in lib.rc_last_error()
+    # ... one token-block less fits (T = 63 * 1024: 2 * 64512 * 16384 < 2^31 - 1)
+    assert _req(_cfg(**dict(big, seq_len=1024), micro_batch=63))[0] == L.RC_OK
+    # the largest weight, hidden x ffn x 2 bytes = 2^31
+    st = _req(_cfg(dtype=L.RC_BF16, hidden=16384, heads=128, ffn=65536, seq_len=8,
+                   max_stashed_mb=1, max_inflight_mb=1))[0]
+    assert st == L.RC_ERR_UNSUPPORTED and b"weight" in lib.rc_last_error()
+    # one head's materialised probabilities (head_dim 64: no fused attention), 2 s^2 bytes
+    st = _req(_cfg(dtype=L.RC_BF16, hidden=256, heads=4, ffn=256, seq_len=32768, max_stashed_mb=1,
+                   max_inflight_mb=1))[0]
+    assert st == L.RC_ERR_UNSUPPORTED and b"probabilities" in lib.rc_last_error()
+    assert _req(_cfg(dtype=L.RC_BF16, hidden=256, heads=4, ffn=256, seq_len=32760, max_stashed_mb=1,
+                     max_inflight_mb=1))[0] == L.RC_OK
+    # fp32 stages do not use the descriptors
+    assert _req(_cfg(**dict(big, dtype=L.RC_FP32), micro_batch=32))[0] == L.RC_OK
+
+
+def test_attention_kernel_query_on_dry_run_handles():
+    lib_or_skip()
+    from paper_2405_14009_amd import Stage
+    kw = dict(num_layers=1, ffn=256, micro_batch=1, dry_run=True)
+    assert Stage(hidden=256, heads=4, seq_len=128, dtype="f32", **kw).attention_kernels() == "materialised"
+    assert Stage(hidden=256, heads=4, seq_len=128, dtype="bf16", **kw).attention_kernels() == "materialised"
+    assert Stage(hidden=256, heads=2, seq_len=128, dtype="bf16", causal=False,
+                 **kw).attention_kernels() == "block"
+    # a small causal grid (one workgroup per compute unit at most) takes the paired kernels
+    assert Stage(hidden=256, heads=2, seq_len=128, dtype="bf16", **kw).attention_kernels() == "paired"
+
+
 def test_bf16_state_holds_weight_copies():
     L, _ = lib_or_skip()
     _, s32, _, _ = _req(_cfg(dtype=L.RC_FP32))

@@ -10,12 +10,14 @@ positions depends only on x[:t0]; and with dy zero beyond t0, dx and every
 weight gradient equal those of the length-t0 prefix.  The GPU always runs the
 full sequence length, i.e. the launch configuration the benchmark times.
 """
+import functools
+
 import numpy as np
 import pytest
 
 import oracle
 from synth import CONFIGS, TEST_CONFIGS, MB, gen_dy, gen_params, gen_x, get_config, op_list
-from tests.conftest import rel_l2
+from tests.conftest import compare_grads, rel_l2
 from tests.gpu_harness import log, run_gpu
 
 pytestmark = pytest.mark.gpu
@@ -123,6 +125,42 @@ def test_attention_variants_parity(variant):
     zero_init = {(l, p) for l in range(cfg.layers) for p in (1, 3, 5, 7, 9, 11)} if not cfg.perturbed else set()
     worst = compare_state(cfg, g, o, t, zero_init)
     log(f"[attn] {variant}: worst state rel-L2 {worst:.2e}")
+
+
+@pytest.mark.parametrize("seq", [1024, 1000])
+def test_causal_block_attention_parity(seq):
+    """Causal attention through the per-query-block kernels (the path of the
+    40-head 13B stage): the grid of query-block pairs would fill its last
+    round of compute units poorly, so each block of 128 queries is one
+    workgroup walking its own causal key range (2 .. 16 key blocks of 64,
+    with the online softmax rescaled across them).  Every output, and every
+    128-query block of y and dx on its own, against the oracle."""
+    from paper_2405_14009_amd import Stage
+    cfg = get_config("block_bf16").with_(seq=seq)
+    stage = Stage.from_config(cfg)
+    path = stage.attention_kernels()
+    log(f"[block attn] s={seq} b={cfg.micro_batch} heads={cfg.heads}: {path} kernels")
+    assert path == "block"
+    params = gen_params(cfg)
+    stage.load_params(params)
+    g = run_gpu(cfg, stage=stage)
+    stage.close()
+    o = oracle.run_oplist(cfg, params=params)
+    t = tol(cfg)
+    assert g.log == [tuple(r) for r in o.stage.log]
+    worst = 0.0
+    for mb in o.y:
+        for name, a, b in (("y", g.y[mb], o.y[mb]), ("dx", g.dx[mb], o.dx[mb])):
+            assert rel_l2(a, b) < t, (name, mb, rel_l2(a, b))
+            for sq in range(cfg.micro_batch):
+                for r0 in range(0, cfg.seq, 128):
+                    e = rel_l2(a[sq, r0:r0 + 128], b[sq, r0:r0 + 128])
+                    worst = max(worst, e)
+                    assert e < t, (name, mb, sq, r0, e)
+    log(f"[block attn] s={seq}: worst per-block rel-L2 of y, dx {worst:.2e}")
+    worst = compare_state(cfg, g, o, t)
+    check_adam_on_gpu_grads(cfg, g, params)
+    log(f"[block attn] s={seq}: worst state rel-L2 {worst:.2e}")
 
 
 def test_w_order_and_determinism():
@@ -251,6 +289,13 @@ def test_staggered_two_stages():
 T0 = 64
 
 
+@functools.lru_cache(maxsize=None)
+def full_params(name):
+    """Seeded parameters of a full-size workload, generated once per session
+    (tens of seconds for the larger stages); callers must not modify them."""
+    return gen_params(CONFIGS[name])
+
+
 @pytest.mark.parametrize("name", ["gpt1.3b", "gpt6.7b", "gpt13b", "gpt175b"])
 def test_fullsize_prefix_parity(name):
     _fullsize(name, batched=False)
@@ -268,7 +313,7 @@ def _fullsize(name, batched):
     cfg = CONFIGS[name]
     log(f"[fullsize] {name}: L={cfg.layers} h={cfg.hidden} a={cfg.heads} f={cfg.ffn} "
         f"s={cfg.seq} b={cfg.micro_batch} n_mb={cfg.n_mb}, prefix t0={T0}")
-    params = gen_params(cfg)
+    params = full_params(name)
     ops = op_list(cfg)
     # 1) real inputs: y[:, :t0] against the oracle forward of the prefix
     pre = cfg.with_(seq=T0)
@@ -297,3 +342,41 @@ def _fullsize(name, batched):
     worst = compare_state(cfg, g, o, 2e-2, zero_init)
     check_adam_on_gpu_grads(cfg, g, params)
     log(f"[fullsize] {name}: worst state rel-L2 {worst:.2e}")
+
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["gpt1.3b", "gpt6.7b", "gpt13b", "gpt175b"])
+def test_fullsize_full_sequence_first_microbatch(name):
+    """The first micro-batch of each full-size op list at its full sequence
+    length, on its own seeded x and dy: F, B_input and B_weight on the GPU
+    (the launch configuration the benchmark times) against the fp64 oracle
+    of the whole sequence; y, dx and every gradient."""
+    import time
+    from paper_2405_14009_amd import RC_READ_GRAD, Stage
+    from synth.schedules import Op
+    cfg = CONFIGS[name]
+    mb = next(o.mb for o in op_list(cfg) if o.kind == "F")
+    log(f"[full seq] {name}: micro-batch {tuple(mb)}, L={cfg.layers} h={cfg.hidden} s={cfg.seq} "
+        f"b={cfg.micro_batch}")
+    params = full_params(name)
+    stage = Stage.from_config(cfg, max_stashed_mb=1, max_inflight_mb=1)
+    log(f"[full seq] {name}: attention kernels {stage.attention_kernels()}")
+    stage.load_params(params)
+    g = run_gpu(cfg, [Op("F", mb), Op("B", mb), Op("W", mb)], stage=stage, read_state=False)
+    grads = stage.read_all(RC_READ_GRAD)
+    stage.close()
+    del stage
+    t0 = time.perf_counter()
+    shp = oracle.LayerShape(cfg.heads, cfg.causal, cfg.ln_eps)
+    ps = [[p.astype(np.float64) for p in layer] for layer in params]
+    yo, caches = oracle.stage_forward(gen_x(cfg, mb.j, mb.k).astype(np.float64), ps, shp)
+    dxo, stashes = oracle.stage_backward_input(gen_dy(cfg, mb.j, mb.k).astype(np.float64), caches, ps)
+    del caches, ps
+    go = oracle.stage_backward_weight(stashes)
+    del stashes
+    log(f"[full seq] {name}: oracle {time.perf_counter() - t0:.1f} s")
+    ey, edx = rel_l2(g.y[tuple(mb)], yo), rel_l2(g.dx[tuple(mb)], dxo)
+    eg = compare_grads(cfg, grads, go, 2e-2)
+    log(f"[full seq] {name}: rel-L2 y {ey:.2e}, dx {edx:.2e}, worst gradient {eg:.2e}")
+    assert ey < 2e-2 and edx < 2e-2, (ey, edx)

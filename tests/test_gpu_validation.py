@@ -6,7 +6,7 @@ import pytest
 
 import oracle
 from synth import MB, gen_dy, gen_params, gen_x, get_config, op_list
-from tests.conftest import rel_l2
+from tests.conftest import compare_grads, rel_l2
 from tests.gpu_harness import log, run_gpu, to_device
 
 pytestmark = pytest.mark.gpu
@@ -180,7 +180,8 @@ def test_executor_under_a_stash_limit_matches_the_deferred_run(slots):
     """Coupled backward passes and early weight passes only reorder the
     gradient sum: same gradients (fp32 sums in another order: <= 1e-6) and the
     same outputs as the fully deferred run, with the stash kept under the
-    limit; and the oracle agrees."""
+    limit; and the limited run's outputs and gradients match the oracle's run
+    of the same op list."""
     from paper_2405_14009_amd import RC_READ_GRAD, Stage
     from paper_2405_14009_amd.executor import execute
     cfg = get_config("small_bf16").with_(n_mb=6)
@@ -212,6 +213,12 @@ def test_executor_under_a_stash_limit_matches_the_deferred_run(slots):
     for l in range(cfg.layers):
         for p in range(12):
             assert rel_l2(g[l][p], ref_g[l][p]) < 1e-6, (l, p)
+    o = oracle.run_oplist(cfg, ops)
+    for mb in o.y:
+        assert rel_l2(out[("F",) + mb], o.y[mb]) < 2e-2, ("y", mb)
+        assert rel_l2(out[("B",) + mb], o.dx[mb]) < 2e-2, ("dx", mb)
+    worst = compare_grads(cfg, g, o.grads, 2e-2)
+    log(f"[stash limit] slots={slots}: worst gradient rel-L2 against the oracle {worst:.2e}")
 
 
 def test_simulated_peer_op_list_drives_the_stage():
