@@ -152,6 +152,27 @@ rc_status rc_stage_create(const rc_stage_config* cfg, const rc_adam_config* adam
                           int32_t stage_index, int32_t pipeline_id, void* state_arena,
                           void* stash_arena, void* work_arena, void* hip_stream, rc_stage** out);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): as
+ * rc_stage_create, but the work arena is a library-owned array of
+ * RC_STATIC_WORK_BYTES in device memory instead of a caller allocation.  Each
+ * GPU the library runs on holds one such array from the first use of the
+ * library on it until the process ends; the call allocates no device memory.
+ * Every handle created this way on one GPU shares that GPU's array, so their
+ * calls must not overlap in time (one stream, or ordered by the caller):
+ * overlapping calls race on the work memory.  Nothing in it needs to start
+ * at zero; it keeps whatever the last call left there.  state_arena and
+ * stash_arena are the caller's, as for rc_stage_create (no dry run).  The
+ * array belongs to the device that runs hip_stream (NULL: the current device).
+ * Errors: RC_ERR_UNSUPPORTED (the configuration needs more work memory than
+ *         RC_STATIC_WORK_BYTES, see rc_stage_memory_requirements; device index
+ *         above 63), RC_ERR_INVALID_ARG (null arenas, misaligned arenas,
+ *         inconsistent config), RC_ERR_HIP. */
+#define RC_STATIC_WORK_BYTES (96u * 1024u * 1024u)
+rc_status rc_stage_create_static(const rc_stage_config* cfg, const rc_adam_config* adam,
+                                 int32_t stage_index, int32_t pipeline_id, void* state_arena,
+                                 void* stash_arena, void* hip_stream, rc_stage** out);
+
 /* Waits for the handle's stream, then frees the host object (not the arenas). */
 rc_status rc_stage_destroy(rc_stage* st);
 

@@ -17,10 +17,11 @@ RC_OP_F, RC_OP_B, RC_OP_W, RC_OP_STEP, RC_OP_SKIP, RC_OP_ROLLBACK = 0, 1, 2, 3, 
 RC_READ_PARAM, RC_READ_GRAD, RC_READ_ADAM_M, RC_READ_ADAM_V = 0, 1, 2, 3
 RC_NUM_PARAMS = 12
 RC_ATTN_MATERIALISED, RC_ATTN_BLOCK, RC_ATTN_PAIRED = 0, 1, 2
+RC_STATIC_WORK_BYTES = 96 * 1024 * 1024
 
 # Every symbol the header declares, for load checks.
 EXPORTED = (
-    "rc_stage_memory_requirements", "rc_stage_create", "rc_stage_destroy", "rc_stage_load_param",
+    "rc_stage_memory_requirements", "rc_stage_create", "rc_stage_create_static", "rc_stage_destroy", "rc_stage_load_param",
     "rc_stage_read", "rc_stage_forward", "rc_stage_backward_input", "rc_stage_backward",
     "rc_stage_backward_weight", "rc_stage_stash_account", "rc_stage_set_stash_limit",
     "rc_stage_backward_weight_many", "rc_stage_optimizer_step", "rc_stage_grad_check",
@@ -105,6 +106,8 @@ def load() -> ctypes.CDLL:
         "rc_stage_memory_requirements": [cfgp, sz, sz, sz],
         "rc_stage_create": [cfgp, ctypes.POINTER(RcAdamConfig), I32, I32, P, P, P, P,
                             ctypes.POINTER(P)],
+        "rc_stage_create_static": [cfgp, ctypes.POINTER(RcAdamConfig), I32, I32, P, P, P,
+                                   ctypes.POINTER(P)],
         "rc_stage_destroy": [P],
         "rc_stage_load_param": [P, I32, I32, P],
         "rc_stage_read": [P, I32, I32, I32, P],

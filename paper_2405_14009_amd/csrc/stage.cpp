@@ -18,6 +18,7 @@
 #include <cmath>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <string>
 #include <utility>
 #include <vector>
@@ -687,30 +688,45 @@ rc_status check_param(rc_stage* st, int layer, int pid) {
   return RC_OK;
 }
 
-}  // namespace
+// Work memory of handles made by rc_stage_create_static: one file-scope
+// device array, which every GPU the library runs on holds until the process
+// ends.  In host code `scratch` names a host-side stand-in, so its device
+// address is looked up once per device (hipGetSymbolAddress, with that
+// device current) and only that address is handed to kernels.
+constexpr size_t kScratchBytes = (size_t)RC_STATIC_WORK_BYTES;
+static __device__ __align__(256) char scratch[kScratchBytes];
 
-extern "C" {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
 
-rc_status rc_stage_memory_requirements(const rc_stage_config* cfg, size_t* state_bytes,
-                                       size_t* stash_bytes, size_t* work_bytes) {
-  if (!state_bytes || !stash_bytes || !work_bytes) return fail(RC_ERR_INVALID_ARG, "null output pointer");
-  Layout y;
-  rc_status r = make_layout(cfg, y);
-  if (r != RC_OK) return r;
-  *state_bytes = y.state_bytes;
-  *stash_bytes = y.stash_bytes;
-  *work_bytes = y.work_bytes;
+// Device address of `scratch` on the device that runs `stream` (the null
+// stream: the current device).
+rc_status scratch_address(hipStream_t stream, void** out) {
+  int cur = 0;
+  HIPCHK(hipGetDevice(&cur));
+  const int dev = stream ? hipGetStreamDeviceId(stream) : cur;
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(RC_ERR_UNSUPPORTED, "no-allocation work memory: device index " + std::to_string(dev) +
+                                        " outside 0.." + std::to_string(kMaxDevices - 1));
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    if (dev != cur) HIPCHK(hipSetDevice(dev));
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) HIPCHK(hipSetDevice(cur));
+    if (e != hipSuccess || !p)
+      return fail(RC_ERR_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
   return RC_OK;
 }
 
-rc_status rc_stage_create(const rc_stage_config* cfg, const rc_adam_config* adam,
-                          int32_t stage_index, int32_t pipeline_id, void* state_arena,
-                          void* stash_arena, void* work_arena, void* hip_stream, rc_stage** out) {
-  if (!out || !adam) return fail(RC_ERR_INVALID_ARG, "null argument");
-  *out = nullptr;
-  Layout y;
-  rc_status r = make_layout(cfg, y);
-  if (r != RC_OK) return r;
+// Shared by rc_stage_create and rc_stage_create_static once the arenas are known.
+rc_status create_handle(const Layout& y, const rc_stage_config* cfg, const rc_adam_config* adam,
+                        int32_t stage_index, int32_t pipeline_id, void* state_arena, void* stash_arena,
+                        void* work_arena, void* hip_stream, rc_stage** out) {
   const bool dry = !state_arena && !stash_arena && !work_arena;
   if (!dry) {
     if (!state_arena || !stash_arena || !work_arena)
@@ -742,6 +758,54 @@ rc_status rc_stage_create(const rc_stage_config* cfg, const rc_adam_config* adam
   }
   *out = st;
   return RC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rc_status rc_stage_memory_requirements(const rc_stage_config* cfg, size_t* state_bytes,
+                                       size_t* stash_bytes, size_t* work_bytes) {
+  if (!state_bytes || !stash_bytes || !work_bytes) return fail(RC_ERR_INVALID_ARG, "null output pointer");
+  Layout y;
+  rc_status r = make_layout(cfg, y);
+  if (r != RC_OK) return r;
+  *state_bytes = y.state_bytes;
+  *stash_bytes = y.stash_bytes;
+  *work_bytes = y.work_bytes;
+  return RC_OK;
+}
+
+rc_status rc_stage_create(const rc_stage_config* cfg, const rc_adam_config* adam,
+                          int32_t stage_index, int32_t pipeline_id, void* state_arena,
+                          void* stash_arena, void* work_arena, void* hip_stream, rc_stage** out) {
+  if (!out || !adam) return fail(RC_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  Layout y;
+  rc_status r = make_layout(cfg, y);
+  if (r != RC_OK) return r;
+  return create_handle(y, cfg, adam, stage_index, pipeline_id, state_arena, stash_arena, work_arena,
+                       hip_stream, out);
+}
+
+rc_status rc_stage_create_static(const rc_stage_config* cfg, const rc_adam_config* adam,
+                                 int32_t stage_index, int32_t pipeline_id, void* state_arena,
+                                 void* stash_arena, void* hip_stream, rc_stage** out) {
+  if (!out || !adam) return fail(RC_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  Layout y;
+  rc_status r = make_layout(cfg, y);
+  if (r != RC_OK) return r;
+  if (y.work_bytes > kScratchBytes)
+    return fail(RC_ERR_UNSUPPORTED, "the configuration needs " + std::to_string(y.work_bytes) +
+                                        " bytes of work memory; the no-allocation work memory holds " +
+                                        std::to_string(kScratchBytes));
+  if (!state_arena || !stash_arena) return fail(RC_ERR_INVALID_ARG, "null state or stash arena");
+  void* work = nullptr;
+  r = scratch_address((hipStream_t)hip_stream, &work);
+  if (r != RC_OK) return r;
+  return create_handle(y, cfg, adam, stage_index, pipeline_id, state_arena, stash_arena, work, hip_stream,
+                       out);
 }
 
 rc_status rc_stage_destroy(rc_stage* st) {

@@ -9,6 +9,13 @@ Inputs (CSV files written by ``rocprofv3 --output-format csv``):
                  (plain 1 GiB device copies), which calibrate them: the
                  factor is (bytes the copy must move) / (bytes the counter
                  reports), applied to every kernel's reading.
+  --mfma         ``*_counter_collection.csv`` of a ``rocprofv3 --pmc
+                 SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16
+                 GRBM_GUI_ACTIVE`` run of the same command: per kernel class
+                 the matrix-core busy fraction (busy cycles over the 1024
+                 SIMDs' active cycles), the bf16 MFMA flops executed (512 per
+                 MOPS unit) and the sustained shader clock (GRBM_GUI_ACTIVE is
+                 summed over the 8 XCDs, divided by the dispatch duration).
 
 Kernel names map to the stage library's kernel classes (the same classes its
 per-launch profiler reports), so the per-launch averages here can be checked
@@ -111,6 +118,41 @@ def calibrate(path, counter):
     return COPY_BYTES / (kib * 1024.0), kib
 
 
+SIMDS = 1024     # 256 compute units x 4 SIMDs
+XCDS = 8
+FLOP_PER_CLK_SIMD = 1024   # dense bf16 MFMA
+
+
+def mfma_classes(path):
+    """Per kernel class: dispatches, summed duration, MFMA busy cycles, bf16
+    MFMA flops and GUI-active cycles, from one counter pass."""
+    disp = defaultdict(dict)
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            d = disp[r["Dispatch_Id"]]
+            d["name"] = r["Kernel_Name"]
+            d["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+            d[r["Counter_Name"]] = float(r["Counter_Value"])
+    acc = defaultdict(lambda: {"n": 0, "ns": 0.0, "busy": 0.0, "mops": 0.0, "grbm": 0.0})
+    for d in disp.values():
+        if "GRBM_GUI_ACTIVE" not in d or d["ns"] <= 0:
+            continue
+        e = acc[kernel_class(d["name"])]
+        e["n"] += 1
+        e["ns"] += d["ns"]
+        e["busy"] += d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+        e["mops"] += d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)
+        e["grbm"] += d["GRBM_GUI_ACTIVE"]
+    out = {}
+    for k, e in acc.items():
+        cyc = e["grbm"] / XCDS                      # active cycles of one XCD
+        out[k] = {"mfma_busy_pct": round(100 * e["busy"] / (cyc * SIMDS), 2) if cyc else None,
+                  "mfma_bf16_flops_per_dispatch": round(512 * e["mops"] / e["n"]),
+                  "sclk_ghz": round(cyc / e["ns"], 3),
+                  "mfma_bf16_tflops_executed": round(512 * e["mops"] / e["ns"] / 1e3, 1)}
+    return out
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--stats", required=True)
@@ -118,6 +160,7 @@ def main(argv=None) -> int:
     ap.add_argument("--write")
     ap.add_argument("--copy-fetch")
     ap.add_argument("--copy-write")
+    ap.add_argument("--mfma")
     ap.add_argument("--bench", help="bench.py JSON line of the same build")
     ap.add_argument("--command", required=True, help="the commands that produced the inputs")
     ap.add_argument("--title", default="GPT-6.7B-shaped stage iteration")
@@ -154,6 +197,8 @@ def main(argv=None) -> int:
                 traffic[k] = {"fetch_bytes_per_dispatch": fb / nf, "write_bytes_per_dispatch": wb / nw,
                               "bytes_per_dispatch": fb / nf + wb / nw}
 
+    mfma = mfma_classes(a.mfma) if a.mfma else {}
+
     bench = None
     if a.bench:
         with open(a.bench) as f:
@@ -176,6 +221,20 @@ def main(argv=None) -> int:
     for r in sorted(stats, key=lambda r: -r["total_ns"])[:14]:
         L.append(f"| `{short(r['name'])}` | {r['calls']} | {r['avg_ns'] / 1e3:.1f} | "
                  f"{100 * r['total_ns'] / tot:.2f} |")
+    if mfma:
+        L += ["", "Matrix cores (one counter pass: SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_BF16, "
+              "GRBM_GUI_ACTIVE).  Busy % is MFMA busy cycles over the 1024 SIMDs' active cycles; the "
+              "clock is the XCDs' active cycles over the dispatch duration; the peak at that clock is "
+              "1024 SIMDs x 1024 flop/clk x clock:", "",
+              "| kernel class | MFMA busy % | bf16 MFMA TFLOP executed / dispatch | executed TFLOP/s | "
+              "sustained clock (GHz) | dense bf16 peak at that clock (TFLOP/s) |",
+              "|---|---:|---:|---:|---:|---:|"]
+        for k, e in sorted(mfma.items(), key=lambda kv: -cls[kv[0]]["total_ns"] if kv[0] in cls else 0):
+            if not e["mfma_bf16_flops_per_dispatch"]:
+                continue
+            L.append(f"| {k} | {e['mfma_busy_pct']} | {e['mfma_bf16_flops_per_dispatch'] / 1e12:.4f} | "
+                     f"{e['mfma_bf16_tflops_executed']} | {e['sclk_ghz']} | "
+                     f"{SIMDS * FLOP_PER_CLK_SIMD * e['sclk_ghz'] / 1e3:.0f} |")
     if cal:
         L += ["", f"Counter calibration (plain 1 GiB device copies): FETCH_SIZE reads "
               f"{cal['copy_fetch_kib']:.0f} KiB and WRITE_SIZE {cal['copy_write_kib']:.0f} KiB per copy "
@@ -191,6 +250,8 @@ def main(argv=None) -> int:
         e = {"dispatches": c["calls"], "avg_us": round(c["total_ns"] / c["calls"] / 1e3, 2)}
         if k in traffic:
             e.update({kk: round(v) for kk, v in traffic[k].items()})
+        if k in mfma:
+            e.update(mfma[k])
         block["classes"][k] = e
     L += ["", "Machine-readable (read by bench.py; `sources_sha256` is the digest of the kernel "
           "sources these counters were taken with):", "", "```json", json.dumps(block, indent=1), "```", ""]

@@ -34,14 +34,17 @@ class Stage:
     """Stage i = ``stage_index`` of data-parallel pipeline k_s = ``pipeline_id``.
 
     ``dry_run=True`` creates a bookkeeping-only handle (no device memory, no
-    kernels): it validates op lists on the host."""
+    kernels): it validates op lists on the host.  ``static_work=True`` creates
+    the handle with rc_stage_create_static: its work memory is the library's
+    own per-device array, so only the state and stash arenas are allocated
+    here."""
 
     def __init__(self, *, num_layers: int, hidden: int, heads: int, ffn: int, seq_len: int,
                  micro_batch: int, causal: bool = True, dtype: str = "bf16",
                  ln_eps: float = 1e-5, max_stashed_mb: int = 1, max_inflight_mb: Optional[int] = None,
                  lr: float = 1e-4, beta1: float = 0.9, beta2: float = 0.95, eps: float = 1e-8,
                  weight_decay: float = 0.1, stage_index: int = 0, pipeline_id: int = 0,
-                 device=None, stream=None, dry_run: bool = False):
+                 device=None, stream=None, dry_run: bool = False, static_work: bool = False):
         self._lib = L.load()
         self._h = None
         if dtype not in ("bf16", "f32"):
@@ -67,10 +70,12 @@ class Stage:
             if not torch.cuda.is_available():
                 raise RuntimeError("no HIP device: the stage runs only on the GPU")
             self.device = torch.device(device if device is not None else "cuda")
+            sizes = (self.state_bytes, self.stash_bytes) + (() if static_work else (self.work_bytes,))
             self._arenas = [torch.empty(max(n, 256), dtype=torch.uint8, device=self.device)
-                            for n in (self.state_bytes, self.stash_bytes, self.work_bytes)]
+                            for n in sizes]
             self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
-            L.check(self._lib.rc_stage_create(
+            create = self._lib.rc_stage_create_static if static_work else self._lib.rc_stage_create
+            L.check(create(
                 ctypes.byref(self.cfg), ctypes.byref(self.adam), stage_index, pipeline_id,
                 *[ctypes.c_void_p(a.data_ptr()) for a in self._arenas],
                 ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(handle)))

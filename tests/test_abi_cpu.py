@@ -102,6 +102,27 @@ def test_bf16_configs_beyond_the_descriptor_range_are_refused():
     assert _req(_cfg(**dict(big, dtype=L.RC_FP32), micro_batch=32))[0] == L.RC_OK
 
 
+def test_static_work_entry_point_checks_its_limit_and_arenas():
+    """rc_stage_create_static refuses a configuration whose work memory
+    exceeds RC_STATIC_WORK_BYTES before touching any device, and needs the
+    caller's two arenas (no dry run)."""
+    L, lib = lib_or_skip()
+    out = ctypes.c_void_p()
+    adam = L.RcAdamConfig(1e-4, 0.9, 0.95, 1e-8, 0.1)
+    big = _cfg(dtype=L.RC_BF16, num_layers=4, hidden=4096, heads=32, ffn=16384, seq_len=2048,
+               max_stashed_mb=32, max_inflight_mb=1)
+    assert _req(big)[3] > L.RC_STATIC_WORK_BYTES
+    st = lib.rc_stage_create_static(ctypes.byref(big), ctypes.byref(adam), 0, 0, None, None, None,
+                                    ctypes.byref(out))
+    assert st == L.RC_ERR_UNSUPPORTED and b"work memory" in lib.rc_last_error()
+    ok = _cfg(dtype=L.RC_BF16, num_layers=4, hidden=4096, heads=32, ffn=16384, seq_len=2048,
+              max_stashed_mb=16, max_inflight_mb=16)
+    assert _req(ok)[3] <= L.RC_STATIC_WORK_BYTES   # the 6.7B-shaped stage fits
+    st = lib.rc_stage_create_static(ctypes.byref(ok), ctypes.byref(adam), 0, 0, None, None, None,
+                                    ctypes.byref(out))
+    assert st == L.RC_ERR_INVALID_ARG and not out.value
+
+
 def test_attention_kernel_query_on_dry_run_handles():
     lib_or_skip()
     from paper_2405_14009_amd import Stage
