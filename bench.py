@@ -28,6 +28,9 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
 PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+# Dense bf16 MFMA peak per GHz of shader clock: 256 CUs x 4 SIMDs x 1024 flop/clk
+# (2516.6 TFLOP/s at the nominal 2.4 GHz, published as 2.5 PFLOP/s).
+PEAK_PER_GHZ = 256 * 4 * 1024 / 1e3
 METRIC = "stage F/B/W TFLOP/s + % bf16 MFMA peak; micro-batches/sec per stage"
 
 
@@ -95,6 +98,26 @@ def measured_traffic(cfg, kernel_class: str):
     return e["bytes_per_dispatch"], os.path.relpath(path, ROOT)
 
 
+def profile_clocks(cfg) -> dict:
+    """Sustained shader clock (GHz) per kernel class from the committed
+    rocprofv3 counter summary of this workload (GRBM_GUI_ACTIVE over the
+    dispatch time), or {} when there is none or the kernel sources changed."""
+    path = os.path.join(ROOT, "profiles", f"stage_{cfg.name}_kernels.md")
+    if not os.path.exists(path):
+        return {}
+    try:
+        block = json.loads(open(path).read().split("```json", 1)[1].split("```", 1)[0])
+    except (IndexError, ValueError):
+        return {}
+    from paper_2405_14009_amd.profile_summary import sources_digest
+    if block.get("sources_sha256") != sources_digest():
+        return {}
+    out = {k: e["sclk_ghz"] for k, e in block.get("classes", {}).items() if e.get("sclk_ghz")}
+    if out:
+        out["_source"] = os.path.relpath(path, ROOT)
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -103,8 +126,11 @@ def main() -> int:
     ap.add_argument("--config", default="gpt6.7b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--single-w", action="store_true",
-                    help="one weight-pass call per micro-batch instead of merging consecutive "
-                         "weight passes of the op list into one batched call")
+                    help="headline with one weight-pass call per micro-batch instead of merging "
+                         "consecutive weight passes of the op list into one batched call")
+    ap.add_argument("--no-single-w-leg", action="store_true",
+                    help="skip the second leg that times the same op list with one weight-pass "
+                         "call per micro-batch")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run three plain 1 GiB device copies (calibrates the HBM byte "
                          "counters of a profiler run) and exit")
@@ -154,16 +180,19 @@ def main() -> int:
 
     # Deferred weight passes that follow each other in the op list run as one
     # batched call (same gradients and op-log records as one call each).
-    steps_ops = []
-    for op in ops:
-        if (op.kind == "W" and not args.single_w and steps_ops and steps_ops[-1][0] == "W"
-                and len(steps_ops[-1][1]) < 32):
-            steps_ops[-1][1].append(op.mb)
-        else:
-            steps_ops.append((op.kind, [op.mb]))
+    def group(single):
+        out = []
+        for op in ops:
+            if (op.kind == "W" and not single and out and out[-1][0] == "W" and len(out[-1][1]) < 32):
+                out[-1][1].append(op.mb)
+            else:
+                out.append((op.kind, [op.mb]))
+        return out
 
-    def run_step(events=None):
-        for kind, mbs in steps_ops:
+    steps_ops = group(args.single_w)
+
+    def run_step(events=None, plan=None):
+        for kind, mbs in (plan or steps_ops):
             if events is not None:
                 a = torch.cuda.Event(enable_timing=True)
                 a.record()
@@ -280,6 +309,49 @@ def main() -> int:
                            "traffic": traffic, "traffic_source": tsrc,
                            "avg_launch_us": round(1e3 * r["ms"] / r["launches"], 2),
                            "flops_per_launch": r["flops"] / r["launches"]}
+    clocks = profile_clocks(cfg) if profile else {}
+    if profile:
+        for name, e in out["kernels"].items():
+            ghz = clocks.get(name)
+            if ghz and "tflops" in e:
+                e["pct_bf16_peak_at_measured_clock"] = round(100 * e["tflops"] / (PEAK_PER_GHZ * ghz), 2)
+        ghz = clocks.get(dom)
+        rf = out["roofline"]
+        rf["measured_clock_ghz"] = ghz
+        rf["peak_at_measured_clock"] = round(PEAK_PER_GHZ * ghz, 1) if ghz else None
+        rf["frac_at_measured_clock"] = round(rf["achieved"] / (PEAK_PER_GHZ * ghz), 4) if ghz else None
+        rf["clock_source"] = clocks.get("_source")
+    if not args.single_w and not args.no_single_w_leg and any(len(m) > 1 for k, m in steps_ops if k == "W"):
+        # The same op list with one weight-pass call per micro-batch (the unit a
+        # schedule defers into a single bubble): wall time of K steps, then the
+        # same K steps with events for the weight pass and its GEMM class.
+        plan = group(True)
+        for _ in range(max(1, args.warmup)):
+            run_step(plan=plan)
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        for _ in range(args.steps):
+            run_step(plan=plan)
+        torch.cuda.synchronize()
+        wall1 = time.perf_counter() - t2
+        leg = {"ms_per_step": round(1e3 * wall1 / args.steps, 3),
+               "value": round(it_flops * args.steps / wall1 / 1e12, 2),
+               "weight_pass_calls_per_step": sum(1 for k, _ in plan if k == "W")}
+        if profile:
+            ev = []
+            stage.profile_enable(True)
+            for _ in range(args.steps):
+                run_step(ev, plan=plan)
+            torch.cuda.synchronize()
+            wms = sum(a.elapsed_time(b) for kind, a, b, _ in ev if kind == "W")
+            leg["w_pass_tflops"] = round(cfg.layers * cfg.n_mb * args.steps * W / (wms / 1e3) / 1e12, 2)
+            r = stage.profile_read()["gemm_wgrad"]
+            stage.profile_enable(False)
+            leg["gemm_wgrad"] = {"launches": r["launches"], "avg_us": round(1e3 * r["ms"] / r["launches"], 2),
+                                 "tflops": round(r["flops"] / (r["ms"] / 1e3) / 1e12, 2)}
+            leg["gemm_wgrad"]["pct_bf16_peak"] = round(100 * leg["gemm_wgrad"]["tflops"] / PEAK_BF16_TFLOPS, 2)
+        out["single_w_leg"] = leg
+        log(f"single weight-pass leg: {leg}")
     if not args.no_cpu_baseline:
         log("timing the fp64 CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(cfg, params)
