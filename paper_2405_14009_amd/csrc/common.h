@@ -25,12 +25,13 @@ __device__ __forceinline__ float gelu_sig(float u) {
 
 __device__ __forceinline__ float gelu_f(float u) { return u * gelu_sig(u); }
 
-// d/du gelu(u) = s + 2 u s (1 - s) z'(u), s = 0.5 (1 + tanh z).
-__device__ __forceinline__ float gelu_grad_f(float u) {
+// d/du gelu(u) = s + 2 u s (1 - s) z'(u), s = 0.5 (1 + tanh z), given s.
+__device__ __forceinline__ float gelu_grad_s(float u, float s) {
   const float c = 0.7978845608028654f;
-  const float s = gelu_sig(u);
   return s + 2.0f * u * s * (1.0f - s) * c * (1.0f + 3.0f * 0.044715f * u * u);
 }
+
+__device__ __forceinline__ float gelu_grad_f(float u) { return gelu_grad_s(u, gelu_sig(u)); }
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

@@ -19,8 +19,8 @@ enum EpiKind {
   EPI_STORE = 0,       // C = acc                                (activation type)
   EPI_BIAS = 1,        // C = acc + bias[n]
   EPI_BIAS_RESID = 2,  // C = acc + bias[n] + resid[m, n]
-  EPI_BIAS_GELU = 3,   // C = U = acc + bias[n];  C2 = gelu(U)
-  EPI_GELU_BWD = 4,    // C = acc * gelu'(aux[m, n])
+  EPI_BIAS_GELU = 3,   // u = acc + bias[n];  C = gelu'(u), C2 = gelu(u)
+  EPI_GELU_BWD = 4,    // C = acc * aux[m, n]   (aux: the stored gelu'(u))
   EPI_F32_ACC = 5,     // C32 = (accumulate ? C32 : 0) + acc     (fp32 gradient buffers)
   EPI_F32_STORE = 6    // C32 = acc                              (fp32 scores)
 };
@@ -87,12 +87,12 @@ __device__ __forceinline__ void epi_store(const GemmParams& p, E* C, int m, int 
     const E* r = (const E*)p.resid;
     C[i] = from_f32<E>(v + p.bias[n] + to_f32(r[(long)m * p.ld_resid + n]));
   } else if constexpr (EPI == EPI_BIAS_GELU) {
-    float u = v + p.bias[n];
-    C[i] = from_f32<E>(u);
-    ((E*)p.C2)[(long)m * p.ldc2 + n] = from_f32<E>(gelu_f(u));
+    const float u = v + p.bias[n], sg = gelu_sig(u);
+    C[i] = from_f32<E>(gelu_grad_s(u, sg));
+    ((E*)p.C2)[(long)m * p.ldc2 + n] = from_f32<E>(u * sg);
   } else if constexpr (EPI == EPI_GELU_BWD) {
-    const E* u = (const E*)p.aux;
-    C[i] = from_f32<E>(v * gelu_grad_f(to_f32(u[(long)m * p.ld_aux + n])));
+    const E* d = (const E*)p.aux;
+    C[i] = from_f32<E>(v * to_f32(d[(long)m * p.ld_aux + n]));
   } else if constexpr (EPI == EPI_F32_ACC) {
     float* c = (float*)C;
     c[i] = p.accumulate ? c[i] + v : v;
@@ -179,13 +179,16 @@ __device__ __forceinline__ void epi_finish4(const GemmParams& p, void* Cv, int m
       v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
     }
     if constexpr (EPI == EPI_GELU_BWD) {
-      const float4 u = cvt4(in.raw);
-      v.x *= gelu_grad_f(u.x); v.y *= gelu_grad_f(u.y); v.z *= gelu_grad_f(u.z); v.w *= gelu_grad_f(u.w);
+      const float4 d = cvt4(in.raw);
+      v.x *= d.x; v.y *= d.y; v.z *= d.z; v.w *= d.w;
     }
-    st4(C + i, v);
     if constexpr (EPI == EPI_BIAS_GELU) {
-      st4((E*)p.C2 + (long)m * p.ldc2 + n,
-          make_float4(gelu_f(v.x), gelu_f(v.y), gelu_f(v.z), gelu_f(v.w)));
+      const float4 sg = make_float4(gelu_sig(v.x), gelu_sig(v.y), gelu_sig(v.z), gelu_sig(v.w));
+      st4(C + i, make_float4(gelu_grad_s(v.x, sg.x), gelu_grad_s(v.y, sg.y), gelu_grad_s(v.z, sg.z),
+                             gelu_grad_s(v.w, sg.w)));
+      st4((E*)p.C2 + (long)m * p.ldc2 + n, make_float4(v.x * sg.x, v.y * sg.y, v.z * sg.z, v.w * sg.w));
+    } else {
+      st4(C + i, v);
     }
   }
 }

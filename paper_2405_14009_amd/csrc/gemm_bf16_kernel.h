@@ -40,6 +40,8 @@
 // concurrent tiles per XCD share fewer operand panels did (256 x 128 tiles).
 #pragma once
 
+#include <algorithm>
+
 #include "gemm.h"
 #include "mfma_common.h"
 
@@ -247,8 +249,10 @@ __device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][TN], const char* ta, c
 // with vector global accesses.  `sm` is this wave's private LDS region.
 // Epilogues with a per-element input (residual, GeLU input, gradient being
 // accumulated) fetch the next block-row's inputs while the current one is
-// finished, so those loads overlap instead of each costing a round trip.
-template <int EPI, int TN, int I0, int I1>
+// finished, so those loads overlap instead of each costing a round trip
+// (LOOK; without it each block-row's inputs are fetched as it is finished,
+// which needs 32 fewer registers).
+template <int EPI, int TN, int I0, int I1, bool LOOK = true>
 __device__ __forceinline__ void epilogue(const GemmParams& p, f32x16 (&acc)[4][TN], float* sm, int m0,
                                          int n0, int lane, long c_off) {
   constexpr int COLS = 32 * TN, STRIDE = COLS + 8;
@@ -271,7 +275,7 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, f32x16 (&acc)[4][T
       if (m < p.M && n < p.N) dst[q] = epi_fetch4<EPI, bf16>(p, C, m, n);
     }
   };
-  if constexpr (IN) fetch(I0, in[0]);
+  if constexpr (IN && LOOK) fetch(I0, in[0]);
 #pragma unroll
   for (int i = I0; i < I1; ++i) {
     const int cur = (i - I0) & 1;
@@ -284,9 +288,10 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, f32x16 (&acc)[4][T
     // The next block-row's inputs are requested once this row's accumulators
     // are in LDS (their registers are free by then).
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (IN) {
+    if constexpr (IN && LOOK) {
       if (i + 1 < I1) fetch(i + 1, in[cur ^ 1]);
     }
+    if constexpr (IN && !LOOK) fetch(i, in[cur]);
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       const int idx = lane + 64 * q;
@@ -463,6 +468,140 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
   }
   float* sm = (float*)(lds + wave * EPI_BYTES);
   epilogue<EPI, TN, 0, 4>(p, acc, sm, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
+}
+
+// Persistent form of gemm_bf16_kernel (256 x 256 tiles, 8 waves, two-stage
+// ring) for launches of more than one round of tiles.  The grid holds one
+// workgroup per compute unit; workgroup q of XCD x (blockIdx.x = x + 8 q)
+// walks the tiles x * ntiles / 8 + q, + nq, + 2 nq, ... of the same tile order
+// as the one-tile-per-workgroup kernel, so the tiles one XCD runs at a time
+// are the ones that share operand panels in its L2.  Between two tiles the
+// next tile's first k-tile is copied into stage 0 before the finished tile's
+// epilogue runs, and the epilogue stages its rows through LDS above stage 0,
+// so that copy is in flight while the epilogue computes and stores.
+// Requirements (checked by the launcher): batch * heads == 1, ntiles % 8 == 0.
+template <int EPI, bool AK, bool BKC>
+__global__ __launch_bounds__(512) void gemm_bf16_persist_kernel(GemmParams p) {
+  constexpr int BM = 256, BN = 256, NW = 8, BK = 64, NST = 2;
+  constexpr int WN_ = 4, TN = 2, NKS = 4;
+  constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
+  constexpr int STAGE = A_BYTES + B_BYTES;
+  constexpr int NIA = A_BYTES / 1024 / NW, NIB = B_BYTES / 1024 / NW;
+  constexpr int EPI_BYTES = 32 * (32 * TN + 8) * 4;
+  constexpr int LDS_BYTES = NST * STAGE > STAGE + NW * EPI_BYTES ? NST * STAGE : STAGE + NW * EPI_BYTES;
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+  static_assert(ColSums<BN, BK>::RED_BYTES <= NW * EPI_BYTES, "column-sum reduction fits above stage 0");
+  __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave / WN_, wn = wave % WN_;
+  const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
+  const int nx = tiles_m * tiles_n / 8;             // tiles of one XCD
+  const int xcd = blockIdx.x & 7, nq = gridDim.x >> 3;
+  constexpr int GM = 8;
+  const int width = GM * tiles_n;
+  auto tile_of = [&](int i, int& m0, int& n0, int& tm) {
+    const int pid = xcd * nx + i;
+    const int first_m = (pid / width) * GM;
+    const int gsz = min(tiles_m - first_m, GM);
+    tm = first_m + (pid % width) % gsz;
+    m0 = tm * BM;
+    n0 = ((pid % width) / gsz) * BN;
+  };
+
+  const bf16* A = (const bf16*)p.A;
+  const bf16* B = (const bf16*)p.B;
+  const i32x4 ra = make_rsrc(A, 2L * (AK ? (long)p.M * p.lda : (long)p.K * p.lda));
+  const i32x4 rb = make_rsrc(B, 2L * (BKC ? (long)p.N * p.ldb : (long)p.K * p.ldb));
+  const int nk = (p.K + BK - 1) / BK;
+
+  Copier<BM, AK, NIA, NW, BK> ca;
+  Copier<BN, BKC, NIB, NW, BK> cb;
+  FragOffsets<BM, AK, 4, NKS, BK> fa;
+  FragOffsets<BN, BKC, TN, NKS, BK> fb;
+  fa.init(wm * 128, lane, 0);
+  fb.init(wn * (BN / WN_), lane, 0);
+  auto issue = [&](char* st, int k0) {
+    if (p.kseg_len > 0) {
+      const int sg = k0 / p.kseg_len, kin = k0 - sg * p.kseg_len;
+      const i32x4 sa = make_rsrc(p.segA[sg], 2L * (AK ? (long)p.M * p.lda : (long)p.kseg_len * p.lda));
+      const i32x4 sb = make_rsrc(p.segB[sg], 2L * (BKC ? (long)p.N * p.ldb : (long)p.kseg_len * p.ldb));
+      ca.issue(sa, st, wave, p.lda, p.M, kin, p.kseg_len);
+      cb.issue(sb, st + A_BYTES, wave, p.ldb, p.N, kin, p.kseg_len);
+    } else {
+      ca.issue(ra, st, wave, p.lda, p.M, k0, p.K);
+      cb.issue(rb, st + A_BYTES, wave, p.ldb, p.N, k0, p.K);
+    }
+  };
+  constexpr bool CS = !AK && !BKC;
+  const bool cs_on = CS && p.colsum_out != nullptr;
+
+  int i = blockIdx.x >> 3;
+  if (i >= nx) return;
+  int m0, n0, tm;
+  tile_of(i, m0, n0, tm);
+  ca.init(wave, p.lda, m0, lane);
+  cb.init(wave, p.ldb, n0, lane);
+  if (nk > 0) issue(lds, 0);
+  f32x16 acc[4][TN];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][j][r] = 0.f;
+  while (true) {
+    int cs_next = tm;
+    ColSums<BN, BK> cs;
+    if (cs_on) cs.init(threadIdx.x);
+    int sc = 0, si = 1;
+    for (int t = 0; t < nk; ++t) {
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vmcnt<0>();
+      __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+      if (t + 1 < nk) issue(lds + si * STAGE, (t + 1) * BK);
+      const char* st = lds + sc * STAGE;
+      mma_tile<BM, BN, AK, BKC, TN, NKS, BK>(acc, st, st + A_BYTES, fa, fb);
+      if constexpr (CS) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (cs_on && t == cs_next) {
+          cs.tile(st + A_BYTES);
+          cs_next += tiles_m;
+        }
+      }
+      sc ^= 1;
+      si ^= 1;
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();  // every wave is past the last k-tile: both stages are free
+    const int cm0 = m0, cn0 = n0, ctm = tm;
+    const int inext = i + nq;
+    if (inext < nx) {
+      tile_of(inext, m0, n0, tm);
+      ca.init(wave, p.lda, m0, lane);
+      cb.init(wave, p.ldb, n0, lane);
+      if (nk > 0) issue(lds, 0);
+    }
+    char* above = lds + STAGE;
+    if constexpr (CS) {
+      if (cs_on) cs.finish((float*)above, p, ctm, cn0, threadIdx.x);
+    }
+    // (the gradient-accumulating epilogue with its inputs fetched a block-row
+    // ahead does not fit the registers next to the next tile's copy state)
+    epilogue<EPI, TN, 0, 4, EPI != EPI_F32_ACC>(p, acc, (float*)(above + wave * EPI_BYTES), cm0 + wm * 128,
+                                                cn0 + wn * (BN / WN_), lane, 0);
+    if (inext >= nx) break;
+    i = inext;
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[a][j][r] = 0.f;
+  }
 }
 
 // Fragments of one unit (two consecutive k-steps, 2 u and 2 u + 1 of the
@@ -699,6 +838,28 @@ hipError_t launch_bf16_variant(const GemmParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Compute units of the current device (cached per device).
+inline int gemm_device_cus() {
+  static int cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] <= 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+template <bool AK, bool BKC, int EPI>
+hipError_t launch_bf16_persist(const GemmParams& p, hipStream_t s) {
+  const int ntiles = ((p.M + 255) / 256) * ((p.N + 255) / 256);
+  const int per_xcd = std::max(1, gemm_device_cus() / 8);
+  const int nq = std::min(ntiles / 8, per_xcd);
+  hipLaunchKernelGGL((gemm_bf16_persist_kernel<EPI, AK, BKC>), dim3(8 * nq), dim3(512), 0, s, p);
+  return hipGetLastError();
+}
+
 template <bool AK, bool BKC, int EPI>
 hipError_t launch_bf16(const GemmParams& p, hipStream_t s) {
   const long z = (long)p.batch * p.heads;
@@ -714,6 +875,16 @@ hipError_t launch_bf16(const GemmParams& p, hipStream_t s) {
   // measured as fast as its ping-pong form.
   if (p.N <= 128 || cost(256, 128) < cost(256, 256))
     return launch_bf16_pp<128, 2, 3, 4, AK, BKC, EPI>(p, s);
+  // Weight-gradient products of more than one round of tiles run the
+  // persistent kernel: each workgroup's next tile starts copying while the
+  // previous tile's fp32 gradient update runs (measured on the 6.7B stage's
+  // single-micro-batch products: 3-4 % faster; neutral for the forward and
+  // input-gradient products, which keep one tile per workgroup).
+  if constexpr (!AK && !BKC) {
+    const long ntiles = (long)((p.M + 255) / 256) * ((p.N + 255) / 256);
+    if (z == 1 && p.krange == KR_FULL && !p.causal_skip && ntiles % 8 == 0 && ntiles > gemm_device_cus())
+      return launch_bf16_persist<AK, BKC, EPI>(p, s);
+  }
   return launch_bf16_variant<256, 256, 8, 1, 64, 2, AK, BKC, EPI>(p, s);
 }
 

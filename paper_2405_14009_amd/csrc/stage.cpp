@@ -61,7 +61,11 @@ struct WLayer {
 };
 // Byte offsets inside one layer of a forward-only slot.
 struct FLayer {
-  size_t QKV, U, P, bytes;  // P: attention probabilities, or the row log-sum-exp (fused attention)
+  // Dg: gelu'(U) of the FFN, which the FC2 input gradient multiplies by (the
+  // forward stores it instead of U: the same information for B_input, and the
+  // derivative is formed where the fp32 U is at hand).  P: attention
+  // probabilities, or the row log-sum-exp (fused attention).
+  size_t QKV, Dg, P, bytes;
 };
 
 struct Layout {
@@ -177,7 +181,7 @@ rc_status make_layout(const rc_stage_config* c, Layout& y) {
   const size_t ss = (size_t)y.b * y.a * y.s * y.s;
   const size_t rows = (size_t)y.b * y.a * y.s;
   y.fl.QKV = take(T * 3 * h * E);
-  y.fl.U = take(T * f * E);
+  y.fl.Dg = take(T * f * E);
   y.fl.P = take(y.flash ? rows * 4 : ss * E);
   y.fl.bytes = o;
   y.wslot_bytes = (size_t)y.L * w.bytes;
@@ -193,7 +197,7 @@ rc_status make_layout(const rc_stage_config* c, Layout& y) {
   // Logical stash bytes per micro-batch (tensor sizes, no alignment padding):
   // from F to B_input the forward-written part of the weight-pass slot (X, A,
   // O, H, C, G and the LayerNorm statistics) plus the forward-only slot (QKV,
-  // U and the attention row statistics or probabilities); from B_input to
+  // gelu'(U) and the attention row statistics or probabilities); from B_input to
   // B_weight the whole weight-pass slot.
   {
     const uint64_t Th = (uint64_t)T * h, Tf = (uint64_t)T * f, st = 16ull * T;
@@ -257,7 +261,7 @@ struct WPtr {
   float *mu1, *r1, *mu2, *r2;
 };
 struct FPtr {
-  char *QKV, *U, *P;
+  char *QKV, *Dg, *P;
 };
 
 WPtr wptr(rc_stage* st, int slot, int l) {
@@ -272,7 +276,7 @@ WPtr wptr(rc_stage* st, int slot, int l) {
 FPtr fptr(rc_stage* st, int slot, int l) {
   const Layout& y = st->lay;
   char* b = st->stash + y.off_fslots + (size_t)slot * y.fslot_bytes + (size_t)l * y.fl.bytes;
-  return {b + y.fl.QKV, b + y.fl.U, b + y.fl.P};
+  return {b + y.fl.QKV, b + y.fl.Dg, b + y.fl.P};
 }
 
 float* master(rc_stage* st, int l, int pid) {
@@ -463,7 +467,7 @@ rc_status run_forward(rc_stage* st, int ws, int fs, const void* x, void* yout) {
       HIPCHK(ln_forward(E, w.H, master(st, l, RC_P_LN2_G), master(st, l, RC_P_LN2_B), w.C, w.mu2,
                         w.r2, T, y.h, y.eps, s));
     }
-    g = gp(T, f, h, w.C, h, 1, weight(st, l, RC_P_W_1), f, 0, EPI_BIAS_GELU, fl.U, f);
+    g = gp(T, f, h, w.C, h, 1, weight(st, l, RC_P_W_1), f, 0, EPI_BIAS_GELU, fl.Dg, f);
     g.bias = master(st, l, RC_P_B_1);
     g.C2 = w.G;
     g.ldc2 = f;
@@ -493,9 +497,9 @@ rc_status run_backward_input(rc_stage* st, int ws, int fs, const void* dy, void*
     // the residual, also copies it into the stash for the weight pass.
     const bool top = l == L - 1;
     char* const dYl = top ? (char*)dy : w.dY;
-    // dU = (dY W_2^T) * gelu'(U)
+    // dU = (dY W_2^T) * gelu'(U), the derivative stored by the forward
     GemmParams g = gp(T, f, h, dYl, h, 1, weight(st, l, RC_P_W_2), h, 1, EPI_GELU_BWD, w.dU, f);
-    g.aux = fl.U;
+    g.aux = fl.Dg;
     g.ld_aux = f;
     HIPCHK(gemm_lin(st, g, RC_K_GEMM_DGRAD));
     // dC = dU W_1^T
