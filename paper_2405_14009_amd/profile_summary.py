@@ -52,11 +52,17 @@ def sources_digest() -> str:
 
 
 def kernel_class(name: str) -> str:
-    # both bf16 GEMM kernels end their template arguments with (A k-contiguous,
-    # B k-contiguous, epilogue)
-    m = re.search(r"gemm_bf16(?:_pp)?_kernel<[^>]*?(true|false),\s*(true|false),\s*(\d+)>", name)
+    # the one-tile and ping-pong bf16 GEMM kernels end their template arguments
+    # with (A k-contiguous, B k-contiguous, epilogue); the persistent kernel
+    # has them as (epilogue, A k-contiguous, B k-contiguous)
+    m = re.search(r"gemm_bf16_persist_kernel<(\d+),\s*(true|false),\s*(true|false)>", name)
     if m:
-        ak, bk, epi = m.group(1), m.group(2), int(m.group(3))
+        epi, ak, bk = int(m.group(1)), m.group(2), m.group(3)
+    else:
+        m = re.search(r"gemm_bf16(?:_pp)?_kernel<[^>]*?(true|false),\s*(true|false),\s*(\d+)>", name)
+        if m:
+            ak, bk, epi = m.group(1), m.group(2), int(m.group(3))
+    if m:
         if (ak, bk) == ("false", "false"):
             return "gemm_wgrad"
         if epi in (1, 2, 3):          # bias / bias + residual / bias + GeLU: the forward products
