@@ -154,8 +154,11 @@ def mfma_classes(path):
         cyc = e["grbm"] / XCDS                      # active cycles of one XCD
         out[k] = {"mfma_busy_pct": round(100 * e["busy"] / (cyc * SIMDS), 2) if cyc else None,
                   "mfma_bf16_flops_per_dispatch": round(512 * e["mops"] / e["n"]),
-                  "sclk_ghz": round(cyc / e["ns"], 3),
                   "mfma_bf16_tflops_executed": round(512 * e["mops"] / e["ns"] / 1e3, 1)}
+        # the counter window exceeds the dispatch by a few microseconds, so the
+        # clock is only read off dispatches that run 40 us or more
+        if e["ns"] / e["n"] >= 40e3:
+            out[k]["sclk_ghz"] = round(cyc / e["ns"], 3)
     return out
 
 
@@ -236,7 +239,7 @@ def main(argv=None) -> int:
               "sustained clock (GHz) | dense bf16 peak at that clock (TFLOP/s) |",
               "|---|---:|---:|---:|---:|---:|"]
         for k, e in sorted(mfma.items(), key=lambda kv: -cls[kv[0]]["total_ns"] if kv[0] in cls else 0):
-            if not e["mfma_bf16_flops_per_dispatch"]:
+            if not e["mfma_bf16_flops_per_dispatch"] or "sclk_ghz" not in e:
                 continue
             L.append(f"| {k} | {e['mfma_busy_pct']} | {e['mfma_bf16_flops_per_dispatch'] / 1e12:.4f} | "
                      f"{e['mfma_bf16_tflops_executed']} | {e['sclk_ghz']} | "
