@@ -155,9 +155,10 @@ def mfma_classes(path):
         out[k] = {"mfma_busy_pct": round(100 * e["busy"] / (cyc * SIMDS), 2) if cyc else None,
                   "mfma_bf16_flops_per_dispatch": round(512 * e["mops"] / e["n"]),
                   "mfma_bf16_tflops_executed": round(512 * e["mops"] / e["ns"] / 1e3, 1)}
-        # the counter window exceeds the dispatch by a few microseconds, so the
-        # clock is only read off dispatches that run 40 us or more
-        if e["ns"] / e["n"] >= 40e3:
+        # the counter window exceeds a dispatch by microseconds, so the clock is
+        # read only off the matrix-core classes' dispatches of 40 us or more
+        # (the classes whose peak it scales)
+        if e["mops"] > 0 and e["ns"] / e["n"] >= 40e3:
             out[k]["sclk_ghz"] = round(cyc / e["ns"], 3)
     return out
 
