@@ -16,6 +16,14 @@ Inputs (CSV files written by ``rocprofv3 --output-format csv``):
                  SIMDs' active cycles), the bf16 MFMA flops executed (512 per
                  MOPS unit) and the sustained shader clock (GRBM_GUI_ACTIVE is
                  summed over the 8 XCDs, divided by the dispatch duration).
+  --l2 / --l2-copy  ``*_counter_collection.csv`` of ``rocprofv3 --pmc
+                 TCP_TCC_READ_REQ_sum TCP_TCC_READ_REQ_LATENCY_sum TCC_HIT_sum
+                 TCC_MISS_sum GRBM_GUI_ACTIVE`` runs of the stage and of the
+                 copy probe: per kernel class the L2 hit rate, the average
+                 L1->L2 read latency, the read requests in flight per compute
+                 unit (summed latency over active cycles) and the bytes per
+                 clock each compute unit receives (request size calibrated on
+                 the copy, whose reads are known).
 
 Kernel names map to the stage library's kernel classes (the same classes its
 per-launch profiler reports), so the per-launch averages here can be checked
@@ -124,6 +132,7 @@ def calibrate(path, counter):
     return COPY_BYTES / (kib * 1024.0), kib
 
 
+CUS = 256
 SIMDS = 1024     # 256 compute units x 4 SIMDs
 XCDS = 8
 FLOP_PER_CLK_SIMD = 1024   # dense bf16 MFMA
@@ -163,6 +172,48 @@ def mfma_classes(path):
     return out
 
 
+def l2_classes(path, copy_path=None):
+    """Per kernel class from one L2 counter pass (see --l2)."""
+    disp = defaultdict(dict)
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            d = disp[r["Dispatch_Id"]]
+            d["name"] = r["Kernel_Name"]
+            d[r["Counter_Name"]] = float(r["Counter_Value"])
+    req_bytes = None
+    if copy_path:
+        reqs = [v for n, v in read_counter(copy_path, "TCP_TCC_READ_REQ_sum")
+                if kernel_class(n) == "copy" or "elementwise" in n]
+        if reqs:
+            big = max(reqs)
+            sel = [v for v in reqs if v > 0.5 * big]
+            req_bytes = COPY_BYTES / (sum(sel) / len(sel))
+    acc = defaultdict(lambda: defaultdict(float))
+    for d in disp.values():
+        if "GRBM_GUI_ACTIVE" not in d:
+            continue
+        e = acc[kernel_class(d["name"])]
+        for c in ("TCP_TCC_READ_REQ_sum", "TCP_TCC_READ_REQ_LATENCY_sum", "TCC_HIT_sum", "TCC_MISS_sum",
+                  "GRBM_GUI_ACTIVE"):
+            e[c] += d.get(c, 0.0)
+    out = {}
+    for k, e in acc.items():
+        req, lat = e["TCP_TCC_READ_REQ_sum"], e["TCP_TCC_READ_REQ_LATENCY_sum"]
+        cyc = e["GRBM_GUI_ACTIVE"] / XCDS
+        hm = e["TCC_HIT_sum"] + e["TCC_MISS_sum"]
+        if not req or not cyc:
+            continue
+        o = {"l2_hit_pct": round(100 * e["TCC_HIT_sum"] / hm, 1) if hm else None,
+             "l1_l2_read_latency_cycles": round(lat / req, 1),
+             "read_requests_in_flight_per_cu": round(lat / (cyc * CUS), 1),
+             "read_requests_per_clk_per_cu": round(req / (cyc * CUS), 3)}
+        if req_bytes:
+            o["read_request_bytes"] = round(req_bytes, 1)
+            o["read_bytes_per_clk_per_cu"] = round(req * req_bytes / (cyc * CUS), 2)
+        out[k] = o
+    return out
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--stats", required=True)
@@ -171,6 +222,8 @@ def main(argv=None) -> int:
     ap.add_argument("--copy-fetch")
     ap.add_argument("--copy-write")
     ap.add_argument("--mfma")
+    ap.add_argument("--l2")
+    ap.add_argument("--l2-copy")
     ap.add_argument("--bench", help="bench.py JSON line of the same build")
     ap.add_argument("--command", required=True, help="the commands that produced the inputs")
     ap.add_argument("--title", default="GPT-6.7B-shaped stage iteration")
@@ -208,6 +261,7 @@ def main(argv=None) -> int:
                               "bytes_per_dispatch": fb / nf + wb / nw}
 
     mfma = mfma_classes(a.mfma) if a.mfma else {}
+    l2 = l2_classes(a.l2, a.l2_copy) if a.l2 else {}
 
     bench = None
     if a.bench:
@@ -245,6 +299,18 @@ def main(argv=None) -> int:
             L.append(f"| {k} | {e['mfma_busy_pct']} | {e['mfma_bf16_flops_per_dispatch'] / 1e12:.4f} | "
                      f"{e['mfma_bf16_tflops_executed']} | {e['sclk_ghz']} | "
                      f"{SIMDS * FLOP_PER_CLK_SIMD * e['sclk_ghz'] / 1e3:.0f} |")
+    if l2:
+        L += ["", "L1 -> L2 reads (one counter pass: TCP_TCC_READ_REQ_sum, TCP_TCC_READ_REQ_LATENCY_sum, "
+              "TCC_HIT_sum, TCC_MISS_sum, GRBM_GUI_ACTIVE).  In flight = summed request latency over the "
+              "256 compute units' active cycles; bytes per clock use the request size measured on the copy "
+              "probe:", "",
+              "| kernel class | L2 hit % | average L1->L2 read latency (cycles) | read requests in flight per CU "
+              "| read bytes / clk / CU |", "|---|---:|---:|---:|---:|"]
+        for k, e in sorted(l2.items(), key=lambda kv: -cls[kv[0]]["total_ns"] if kv[0] in cls else 0):
+            if k not in cls or cls[k]["total_ns"] < 0.005 * tot:
+                continue
+            L.append(f"| {k} | {e['l2_hit_pct']} | {e['l1_l2_read_latency_cycles']} | "
+                     f"{e['read_requests_in_flight_per_cu']} | {e.get('read_bytes_per_clk_per_cu', '—')} |")
     if cal:
         L += ["", f"Counter calibration (plain 1 GiB device copies): FETCH_SIZE reads "
               f"{cal['copy_fetch_kib']:.0f} KiB and WRITE_SIZE {cal['copy_write_kib']:.0f} KiB per copy "
@@ -262,6 +328,8 @@ def main(argv=None) -> int:
             e.update({kk: round(v) for kk, v in traffic[k].items()})
         if k in mfma:
             e.update(mfma[k])
+        if k in l2:
+            e.update(l2[k])
         block["classes"][k] = e
     L += ["", "Machine-readable (read by bench.py; `sources_sha256` is the digest of the kernel "
           "sources these counters were taken with):", "", "```json", json.dumps(block, indent=1), "```", ""]
