@@ -120,6 +120,13 @@ TEST_CONFIGS = {
         name="block_bf16", layers=1, hidden=1280, heads=10, ffn=2048, seq=1024, micro_batch=4,
         causal=True, dtype="bf16", n_mb=2, rerouted=(1,), schedule="1f1b_deferred_shuffled_w",
         warmup=2, perturbed=True),
+    # Weight-gradient products of more than one round of 256 x 256 tiles with
+    # ragged edges (FC1: [1152, 16200] = 5 x 64 tiles, FC2: 64 x 5), which the
+    # launcher gives to the persistent kernel on a 256-CU device.
+    "persist_bf16": StageConfig(
+        name="persist_bf16", layers=1, hidden=1152, heads=9, ffn=16200, seq=128, micro_batch=2,
+        causal=True, dtype="bf16", n_mb=3, rerouted=(2,), schedule="1f1b_deferred_shuffled_w",
+        warmup=2, perturbed=True),
     "tiny_noncausal": CONFIGS["tiny"].with_(name="tiny_noncausal", causal=False),
     "tiny_perturbed": CONFIGS["tiny"].with_(name="tiny_perturbed", perturbed=True),
 }

@@ -82,9 +82,16 @@ def check_adam_on_gpu_grads(cfg, g, params0, hp=None):
 
 
 @pytest.mark.parametrize("name", ["tiny", "tiny_noncausal", "tiny_perturbed", "small_f32", "small_bf16",
-                                  "wide_bf16"])
+                                  "wide_bf16", "persist_bf16"])
 def test_elementwise_parity(name):
     cfg = get_config(name)
+    if name == "persist_bf16":
+        # FC1 / FC2 weight gradients: 320 tiles of 256 x 256 (ragged), a multiple of 8 and more
+        # than one per compute unit, so the launcher takes the persistent kernel
+        import torch
+        cus = torch.cuda.get_device_properties(0).multi_processor_count
+        tiles = -(-cfg.hidden // 256) * -(-cfg.ffn // 256)
+        assert tiles % 8 == 0 and tiles > cus, (tiles, cus)
     log(f"[parity] {name}: shapes L={cfg.layers} h={cfg.hidden} a={cfg.heads} f={cfg.ffn} "
         f"s={cfg.seq} b={cfg.micro_batch} {cfg.dtype} causal={cfg.causal}")
     g = run_gpu(cfg)
@@ -192,7 +199,8 @@ def _grouped(ops):
     return out
 
 
-@pytest.mark.parametrize("name,seq", [("small_bf16", None), ("small_bf16", 328), ("small_f32", None)])
+@pytest.mark.parametrize("name,seq", [("small_bf16", None), ("small_bf16", 328), ("small_f32", None),
+                                      ("persist_bf16", None)])
 def test_batched_weight_pass(name, seq):
     """One weight pass over several deferred micro-batches (one product per
     parameter over their concatenated tokens; for bf16 token counts that are
