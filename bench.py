@@ -59,19 +59,28 @@ def cpu_baseline(cfg, params) -> dict:
         cores = len(os.sched_getaffinity(0))
     P = [p.astype(np.float64) for p in params[0]]
     shp = oracle.LayerShape(cfg.heads, cfg.causal, cfg.ln_eps)
-    dt, n = 0.0, 0
-    while dt < 10.0 and n < cfg.n_mb:
+    t = {"F": 0.0, "B": 0.0, "W": 0.0}
+    n = 0
+    while sum(t.values()) < 10.0 and n < cfg.n_mb:
         x = gen_x(cfg, n).astype(np.float64)
         dy = gen_dy(cfg, n).astype(np.float64)
         t0 = time.perf_counter()
         y, cache = oracle.layer_forward(x, P, shp)
+        t1 = time.perf_counter()
         dx, ws = oracle.layer_backward_input(dy, cache, P)
+        t2 = time.perf_counter()
         oracle.layer_backward_weight(ws)
-        dt += time.perf_counter() - t0
+        t3 = time.perf_counter()
+        t["F"] += t1 - t0
+        t["B"] += t2 - t1
+        t["W"] += t3 - t2
         n += 1
-    flops = n * sum(cfg.flops_per_layer())
+    F, B, W = cfg.flops_per_layer()
+    flops = n * (F + B + W)
+    dt = sum(t.values())
     return {"value": round(flops / dt / 1e12, 4), "unit": "TFLOP/s", "cores": int(cores),
             "kind": "oracle",
+            "pass_tflops": {k: round(n * fl / t[k] / 1e12, 4) for k, fl in (("F", F), ("B", B), ("W", W))},
             "sample": (f"fp64 numpy oracle: F + B_input + B_weight of 1 of {cfg.layers} layers for {n} of "
                        f"{cfg.n_mb} micro-batches at full shape ({flops / 1e9:.0f} GFLOP algorithmic) "
                        f"in {dt:.1f} s")}
