@@ -86,6 +86,49 @@ def cpu_baseline(cfg, params) -> dict:
                        f"in {dt:.1f} s")}
 
 
+def cpu_baseline_all() -> dict:
+    """The fp64 oracle per workload: F, B_input and B_weight of one
+    micro-batch through all of the stage's layers (the first micro-batch of
+    its op list, full shape), and for the tiny workload its whole op list
+    (every micro-batch and the AdamW step).  Minutes of CPU time; not part of
+    the default run."""
+    import numpy as np
+    import oracle
+    from synth import CONFIGS, gen_dy, gen_params, gen_x, op_list
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    out = {"cores": int(cores), "kind": "oracle", "workloads": {}}
+    for name, cfg in CONFIGS.items():
+        mb = next(o.mb for o in op_list(cfg) if o.kind == "F")
+        ps = [[p.astype(np.float64) for p in layer] for layer in gen_params(cfg)]
+        shp = oracle.LayerShape(cfg.heads, cfg.causal, cfg.ln_eps)
+        x = gen_x(cfg, mb.j, mb.k).astype(np.float64)
+        dy = gen_dy(cfg, mb.j, mb.k).astype(np.float64)
+        t0 = time.perf_counter()
+        y, caches = oracle.stage_forward(x, ps, shp)
+        t1 = time.perf_counter()
+        dx, stashes = oracle.stage_backward_input(dy, caches, ps)
+        t2 = time.perf_counter()
+        del caches
+        oracle.stage_backward_weight(stashes)
+        t3 = time.perf_counter()
+        F, B, W = (cfg.layers * f for f in cfg.flops_per_layer())
+        e = {"F_s": round(t1 - t0, 3), "B_s": round(t2 - t1, 3), "W_s": round(t3 - t2, 3),
+             "tflops": {"F": round(F / (t1 - t0) / 1e12, 4), "B": round(B / (t2 - t1) / 1e12, 4),
+                        "W": round(W / (t3 - t2) / 1e12, 4)}}
+        if name == "tiny":
+            t4 = time.perf_counter()
+            oracle.run_oplist(cfg)
+            e["op_list_s"] = round(time.perf_counter() - t4, 3)
+        out["workloads"][name] = e
+        log(f"cpu baseline {name}: {e}")
+        del ps, stashes
+    return out
+
+
 def measured_traffic(cfg, kernel_class: str):
     """HBM bytes per launch of a kernel class from the committed rocprofv3
     counter summary of this workload (FETCH_SIZE + WRITE_SIZE, copy-calibrated),
@@ -145,7 +188,13 @@ def main() -> int:
                          "counters of a profiler run) and exit")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the per-kernel events (for external profilers)")
+    ap.add_argument("--cpu-baseline-all", action="store_true",
+                    help="only time the fp64 oracle on one micro-batch of every workload (and the "
+                         "tiny op list) and print it as JSON; no device work")
     args = ap.parse_args()
+    if args.cpu_baseline_all:
+        print(json.dumps(cpu_baseline_all()), flush=True)
+        return 0
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one stage on one GPU; the library runs no collectives, so there "
               "is no multi-GPU run to measure (use --gpus 1)", file=sys.stderr)
