@@ -960,26 +960,13 @@ AttnArgs make_args(const void* qkv, int b, int s, int heads, int h) {
   return a;
 }
 
-// Compute units of the current device (cached per device).
-int device_cus() {
-  static int cache[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cache[dev] <= 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cache[dev] = n;
-  }
-  return cache[dev];
-}
-
 // The paired kernels run one equal-length workgroup per CU.  They are used
 // when those workgroups fill the CUs of their last round to 90 % or more, or
 // when there are so few that every CU holds at most one anyway (a small
 // problem); otherwise the per-block kernels, whose uneven blocks the
 // hardware packs two to a CU, lose less to the last round.
 bool pair_grid_fills(long wgs) {
-  const long cus = device_cus();
+  const long cus = device_compute_units();
   if (2 * wgs <= cus) return true;
   const long rounds = (wgs + cus - 1) / cus;
   return 10 * wgs >= 9 * rounds * cus;

@@ -72,3 +72,17 @@ __device__ __forceinline__ float block_max(float v, float* red) {
   for (int i = 1; i < NT / 64; ++i) s = fmaxf(s, red[i]);
   return s;
 }
+
+// Compute units of the current device (host; cached per device, 256 when the
+// query fails).
+inline int device_compute_units() {
+  static int cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] <= 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}

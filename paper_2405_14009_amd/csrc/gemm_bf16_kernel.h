@@ -838,23 +838,10 @@ hipError_t launch_bf16_variant(const GemmParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Compute units of the current device (cached per device).
-inline int gemm_device_cus() {
-  static int cache[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cache[dev] <= 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cache[dev] = n;
-  }
-  return cache[dev];
-}
-
 template <bool AK, bool BKC, int EPI>
 hipError_t launch_bf16_persist(const GemmParams& p, hipStream_t s) {
   const int ntiles = ((p.M + 255) / 256) * ((p.N + 255) / 256);
-  const int per_xcd = std::max(1, gemm_device_cus() / 8);
+  const int per_xcd = std::max(1, device_compute_units() / 8);
   const int nq = std::min(ntiles / 8, per_xcd);
   hipLaunchKernelGGL((gemm_bf16_persist_kernel<EPI, AK, BKC>), dim3(8 * nq), dim3(512), 0, s, p);
   return hipGetLastError();
@@ -882,7 +869,7 @@ hipError_t launch_bf16(const GemmParams& p, hipStream_t s) {
   // input-gradient products, which keep one tile per workgroup).
   if constexpr (!AK && !BKC) {
     const long ntiles = (long)((p.M + 255) / 256) * ((p.N + 255) / 256);
-    if (z == 1 && p.krange == KR_FULL && !p.causal_skip && ntiles % 8 == 0 && ntiles > gemm_device_cus())
+    if (z == 1 && p.krange == KR_FULL && !p.causal_skip && ntiles % 8 == 0 && ntiles > device_compute_units())
       return launch_bf16_persist<AK, BKC, EPI>(p, s);
   }
   return launch_bf16_variant<256, 256, 8, 1, 64, 2, AK, BKC, EPI>(p, s);
