@@ -15,9 +15,10 @@
 // buffer-load-to-LDS instructions (each wave instruction deposits 64 lanes x
 // 16 bytes contiguously; out-of-range offsets deposit zeros, so ragged edges
 // need no branches and no registers hold tile data).  NST stages form a ring:
-// the copy of tile t + NST - 1 is issued when tile t starts; a wave waits only
-// for its own copies of the oldest stage (vmcnt of the copies issued after
-// it), then one barrier per k-tile publishes that stage and frees the one
+// the copy of tile t + NST - 1 is issued while tile t is multiplied, its A
+// and B slices at separate points of the first k-steps; a wave waits only for
+// its own copies of the oldest stage (vmcnt of the copies issued after it),
+// then one barrier per k-tile publishes that stage and frees the one
 // multiplied before.
 //   * k-contiguous operand: LDS tile [rows][BK], 16-byte chunks XOR-swizzled
 //     by row; fragments are one ds_read_b128 per lane.
@@ -88,8 +89,14 @@ struct Copier {
   }
   __device__ __forceinline__ void issue(const i32x4& r, char* tile, int wave, long ld, int MN, int k0,
                                         int K) const {
+    issue_part<0, NI>(r, tile, wave, ld, MN, k0, K);
+  }
+  // slices Q0 .. Q1-1 of this wave's share
+  template <int Q0, int Q1>
+  __device__ __forceinline__ void issue_part(const i32x4& r, char* tile, int wave, long ld, int MN, int k0,
+                                             int K) const {
 #pragma unroll
-    for (int q = 0; q < NI; ++q) {
+    for (int q = Q0; q < Q1; ++q) {
       uint32_t off;
       if (KC) {
         const int k = k0 + kk;
@@ -202,10 +209,15 @@ __device__ __forceinline__ bf16x8 frag(const char* tile, const FragOffsets<ROWS,
 // NKS k-steps.  The fragments of k-step ks+1 are read while the MFMAs of
 // k-step ks issue; scheduling groups pin that interleave (one MFMA, then that
 // k-step's share of LDS reads) so the reads stay ahead of their use.
-template <int BM, int BN, bool AK, bool BKC, int TN, int NKS, int BK>
+// step(ks) runs at the head of k-step ks, after the fragment reads issued
+// before it (the kernels issue their next k-tile's copies from it).
+struct NoStep {
+  __device__ __forceinline__ void operator()(int) const {}
+};
+template <int BM, int BN, bool AK, bool BKC, int TN, int NKS, int BK, typename Step = NoStep>
 __device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][TN], const char* ta, const char* tb,
                                          const FragOffsets<BM, AK, 4, NKS, BK>& fa,
-                                         const FragOffsets<BN, BKC, TN, NKS, BK>& fb) {
+                                         const FragOffsets<BN, BKC, TN, NKS, BK>& fb, Step step = Step()) {
   constexpr int READS = 4 * (AK ? 1 : 2) + TN * (BKC ? 1 : 2);  // LDS read instructions per k-step
   constexpr int NMFMA = 4 * TN;
   constexpr int PER = (READS + NMFMA - 1) / NMFMA;
@@ -218,6 +230,9 @@ __device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][TN], const char* ta, c
 #pragma unroll
   for (int ks = 0; ks < NKS; ++ks) {
     const int c = ks & 1;
+    __builtin_amdgcn_sched_barrier(0);
+    step(ks);
+    __builtin_amdgcn_sched_barrier(0);
     if (ks + 1 < NKS) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) af[c ^ 1][i] = frag(ta, fa, i, ks + 1);
@@ -414,26 +429,38 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
   ColSums<BN, BK> cs;
   if (cs_on) cs.init(threadIdx.x);
 
-  // With a segmented reduction the k-tile's segment selects the operand bases
-  // (a k-tile never straddles segments).
-  auto issue = [&](char* st, int k0) {
+  // Operands of the k-tile at k0: with a segmented reduction the k-tile's
+  // segment selects the operand bases (a k-tile never straddles segments).
+  struct Src {
+    i32x4 a, b;
+    int k, kend;
+  };
+  auto source = [&](int k0) {
+    Src r{ra, rb, k0, ke};
     if (p.kseg_len > 0) {
-      const int sg = k0 / p.kseg_len, kin = k0 - sg * p.kseg_len;
-      const i32x4 sa = make_rsrc((const bf16*)p.segA[sg] + zb * p.a_bs + zh * p.a_hs,
-                                 2L * (AK ? (long)p.M * p.lda : (long)p.kseg_len * p.lda));
-      const i32x4 sb = make_rsrc((const bf16*)p.segB[sg] + zb * p.b_bs + zh * p.b_hs,
-                                 2L * (BKC ? (long)p.N * p.ldb : (long)p.kseg_len * p.ldb));
-      ca.issue(sa, st, wave, p.lda, p.M, kin, p.kseg_len);
-      cb.issue(sb, st + A_BYTES, wave, p.ldb, p.N, kin, p.kseg_len);
-    } else {
-      ca.issue(ra, st, wave, p.lda, p.M, k0, ke);
-      cb.issue(rb, st + A_BYTES, wave, p.ldb, p.N, k0, ke);
+      const int sg = k0 / p.kseg_len;
+      r.k = k0 - sg * p.kseg_len;
+      r.kend = p.kseg_len;
+      r.a = make_rsrc((const bf16*)p.segA[sg] + zb * p.a_bs + zh * p.a_hs,
+                      2L * (AK ? (long)p.M * p.lda : (long)p.kseg_len * p.lda));
+      r.b = make_rsrc((const bf16*)p.segB[sg] + zb * p.b_bs + zh * p.b_hs,
+                      2L * (BKC ? (long)p.N * p.ldb : (long)p.kseg_len * p.ldb));
     }
+    return r;
+  };
+  auto issue = [&](char* st, int k0) {
+    const Src sr = source(k0);
+    ca.issue(sr.a, st, wave, p.lda, p.M, sr.k, sr.kend);
+    cb.issue(sr.b, st + A_BYTES, wave, p.ldb, p.N, sr.k, sr.kend);
   };
   // Ring of NST stages: tile t lives in stage t mod NST.  Tiles 0 .. NST-2 are
   // issued up front; iteration t waits for tile t, publishes it with the
   // barrier (which also certifies that every wave is done with tile t-1), then
-  // refills tile t-1's stage with tile t + NST - 1 and multiplies tile t.
+  // refills tile t-1's stage with tile t + NST - 1 while it multiplies tile t:
+  // the A slices at the head of the first k-step, the B slices at the head of
+  // the second (one burst of all of them ahead of the first MFMAs held those
+  // MFMAs back: 5-11 % longer products).
+  static_assert(NKS >= 2, "the refill spans two k-steps");
 #pragma unroll
   for (int i = 0; i < NST - 1; ++i)
     if (i < nk) issue(lds + i * STAGE, kb + i * BK);
@@ -444,9 +471,14 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
     else wait_vmcnt<0>();
     __syncthreads();
     __builtin_amdgcn_sched_barrier(0);
-    if (t + NST - 1 < nk) issue(lds + si * STAGE, kb + (t + NST - 1) * BK);
+    const bool refill = t + NST - 1 < nk;
+    const Src nx = source(refill ? kb + (t + NST - 1) * BK : kb);
+    char* dst = lds + si * STAGE;
     const char* st = lds + sc * STAGE;
-    mma_tile<BM, BN, AK, BKC, TN, NKS, BK>(acc, st, st + A_BYTES, fa, fb);
+    mma_tile<BM, BN, AK, BKC, TN, NKS, BK>(acc, st, st + A_BYTES, fa, fb, [&](int ks) {
+      if (refill && ks == 0) ca.issue(nx.a, dst, wave, p.lda, p.M, nx.k, nx.kend);
+      if (refill && ks == 1) cb.issue(nx.b, dst + A_BYTES, wave, p.ldb, p.N, nx.k, nx.kend);
+    });
     if constexpr (CS) {
       // while the tile's MFMAs drain; the stage stays valid until the next barrier
       __builtin_amdgcn_sched_barrier(0);
@@ -522,17 +554,25 @@ __global__ __launch_bounds__(512) void gemm_bf16_persist_kernel(GemmParams p) {
   FragOffsets<BN, BKC, TN, NKS, BK> fb;
   fa.init(wm * 128, lane, 0);
   fb.init(wn * (BN / WN_), lane, 0);
-  auto issue = [&](char* st, int k0) {
+  struct Src {
+    i32x4 a, b;
+    int k, kend;
+  };
+  auto source = [&](int k0) {
+    Src r{ra, rb, k0, p.K};
     if (p.kseg_len > 0) {
-      const int sg = k0 / p.kseg_len, kin = k0 - sg * p.kseg_len;
-      const i32x4 sa = make_rsrc(p.segA[sg], 2L * (AK ? (long)p.M * p.lda : (long)p.kseg_len * p.lda));
-      const i32x4 sb = make_rsrc(p.segB[sg], 2L * (BKC ? (long)p.N * p.ldb : (long)p.kseg_len * p.ldb));
-      ca.issue(sa, st, wave, p.lda, p.M, kin, p.kseg_len);
-      cb.issue(sb, st + A_BYTES, wave, p.ldb, p.N, kin, p.kseg_len);
-    } else {
-      ca.issue(ra, st, wave, p.lda, p.M, k0, p.K);
-      cb.issue(rb, st + A_BYTES, wave, p.ldb, p.N, k0, p.K);
+      const int sg = k0 / p.kseg_len;
+      r.k = k0 - sg * p.kseg_len;
+      r.kend = p.kseg_len;
+      r.a = make_rsrc(p.segA[sg], 2L * (AK ? (long)p.M * p.lda : (long)p.kseg_len * p.lda));
+      r.b = make_rsrc(p.segB[sg], 2L * (BKC ? (long)p.N * p.ldb : (long)p.kseg_len * p.ldb));
     }
+    return r;
+  };
+  auto issue = [&](char* st, int k0) {
+    const Src sr = source(k0);
+    ca.issue(sr.a, st, wave, p.lda, p.M, sr.k, sr.kend);
+    cb.issue(sr.b, st + A_BYTES, wave, p.ldb, p.N, sr.k, sr.kend);
   };
   constexpr bool CS = !AK && !BKC;
   const bool cs_on = CS && p.colsum_out != nullptr;
@@ -561,9 +601,15 @@ __global__ __launch_bounds__(512) void gemm_bf16_persist_kernel(GemmParams p) {
       wait_vmcnt<0>();
       __syncthreads();
       __builtin_amdgcn_sched_barrier(0);
-      if (t + 1 < nk) issue(lds + si * STAGE, (t + 1) * BK);
+      // refill split over the first two k-steps as in gemm_bf16_kernel
+      const bool refill = t + 1 < nk;
+      const Src nx = source(refill ? (t + 1) * BK : 0);
+      char* dst = lds + si * STAGE;
       const char* st = lds + sc * STAGE;
-      mma_tile<BM, BN, AK, BKC, TN, NKS, BK>(acc, st, st + A_BYTES, fa, fb);
+      mma_tile<BM, BN, AK, BKC, TN, NKS, BK>(acc, st, st + A_BYTES, fa, fb, [&](int ks) {
+        if (refill && ks == 0) ca.issue(nx.a, dst, wave, p.lda, p.M, nx.k, nx.kend);
+        if (refill && ks == 1) cb.issue(nx.b, dst + A_BYTES, wave, p.ldb, p.N, nx.k, nx.kend);
+      });
       if constexpr (CS) {
         __builtin_amdgcn_sched_barrier(0);
         if (cs_on && t == cs_next) {
@@ -653,13 +699,16 @@ __device__ __forceinline__ void phase_barrier() {
 // wave tiles and multiplies k-steps 2 g, 2 g + 1 of every k-tile (one unit);
 // the two groups' partial sums are added through LDS at the end.  (The unit
 // loop also allows several units per k-tile, as a single k-group would need.)
-// Copies.  Tile t + NST - 1 is issued in the memory phase of tile t's first
-// unit.  Tile t + 1 is first read in group 0's first memory phase of tile
-// t + 1; before the barrier that opens that phase each wave waits for its own
-// share (group 0 after its last compute phase of tile t, group 1 after its
-// last memory phase of tile t).  The stage being refilled held tile t - 1,
-// whose last fragment reads (group 1's last memory phase of tile t - 1)
-// completed before the barrier that opens group 0's first phase of tile t.
+// Copies.  Tile t + NST - 1 is issued in tile t's first unit: in its memory
+// phase ahead of the fragment reads, or, with k-contiguous B tiles, the A
+// slices after the reads and the B slices at the head of the compute phase.
+// Tile t + 1 is first read in group 0's first memory phase of tile t + 1;
+// before the barrier that opens that phase each wave waits for its own share
+// (group 0 after its last compute phase of tile t, group 1 after its last
+// memory phase of tile t, when its B slices of tile t + NST - 1 may not be
+// issued yet).  The stage being refilled held tile t - 1, whose last fragment
+// reads (group 1's last memory phase of tile t - 1) completed before the
+// barrier that opens group 0's first phase of tile t.
 template <int BN, int KS, int NST, int GM, bool AK, bool BKC, int EPI>
 __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
   constexpr int BM = 256, NW = 8, BK = 64;
@@ -742,25 +791,41 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
   ColSums<BN, BK> cs;
   if (cs_on) cs.init(threadIdx.x);
 
-  auto issue = [&](char* st, int k0) {
-    if (p.kseg_len > 0) {
-      const int sg = k0 / p.kseg_len, kin = k0 - sg * p.kseg_len;
-      const i32x4 sa = make_rsrc((const bf16*)p.segA[sg] + zb * p.a_bs + zh * p.a_hs,
-                                 2L * (AK ? (long)p.M * p.lda : (long)p.kseg_len * p.lda));
-      const i32x4 sb = make_rsrc((const bf16*)p.segB[sg] + zb * p.b_bs + zh * p.b_hs,
-                                 2L * (BKC ? (long)p.N * p.ldb : (long)p.kseg_len * p.ldb));
-      ca.issue(sa, st, wave, p.lda, p.M, kin, p.kseg_len);
-      cb.issue(sb, st + A_BYTES, wave, p.ldb, p.N, kin, p.kseg_len);
-    } else {
-      ca.issue(ra, st, wave, p.lda, p.M, k0, ke);
-      cb.issue(rb, st + A_BYTES, wave, p.ldb, p.N, k0, ke);
-    }
+  struct Src {
+    i32x4 a, b;
+    int k, kend;
   };
+  auto source = [&](int k0) {
+    Src r{ra, rb, k0, ke};
+    if (p.kseg_len > 0) {
+      const int sg = k0 / p.kseg_len;
+      r.k = k0 - sg * p.kseg_len;
+      r.kend = p.kseg_len;
+      r.a = make_rsrc((const bf16*)p.segA[sg] + zb * p.a_bs + zh * p.a_hs,
+                      2L * (AK ? (long)p.M * p.lda : (long)p.kseg_len * p.lda));
+      r.b = make_rsrc((const bf16*)p.segB[sg] + zb * p.b_bs + zh * p.b_hs,
+                      2L * (BKC ? (long)p.N * p.ldb : (long)p.kseg_len * p.ldb));
+    }
+    return r;
+  };
+  auto issue = [&](char* st, int k0) {
+    const Src sr = source(k0);
+    ca.issue(sr.a, st, wave, p.lda, p.M, sr.k, sr.kend);
+    cb.issue(sr.b, st + A_BYTES, wave, p.ldb, p.N, sr.k, sr.kend);
+  };
+  // With k-contiguous B tiles (the input-gradient products) the refill's A
+  // slices follow the unit's fragment reads and its B slices open the compute
+  // phase (6-8 % shorter products than one burst ahead of the reads; with
+  // m/n-contiguous B tiles the split measured no faster).
+  constexpr bool SPLIT = BKC;
   // Waits until this wave's share of tile t + 1 has landed (the copies of
-  // tiles t + 2 .. t + NST - 1 may stay in flight).
-  auto wait_next = [&](int t) {
-    if (t + NST - 1 < nk) wait_vmcnt<(NST - 2) * PER_TILE>();
-    else wait_vmcnt<0>();
+  // tiles t + 2 .. t + NST - 1 issued so far may stay in flight: all of them,
+  // or, when group 1 waits in the memory phase of a split refill, all but
+  // the B slices of tile t + NST - 1, which it has not issued yet).
+  auto wait_next = [&](int t, bool b_pending) {
+    if (t + NST - 1 >= nk) wait_vmcnt<0>();
+    else if (b_pending) wait_vmcnt<(NST - 3) * PER_TILE + NIA>();
+    else wait_vmcnt<(NST - 2) * PER_TILE>();
   };
 
   // Prologue: tiles 0 .. NST-2 land before either group starts.
@@ -778,8 +843,15 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       // memory phase
-      if (u == 0 && t + NST - 1 < nk) issue(lds + si * STAGE, kb + (t + NST - 1) * BK);
+      const bool refill = u == 0 && t + NST - 1 < nk;
+      char* dst = lds + si * STAGE;
+      const Src nx = source(refill ? kb + (t + NST - 1) * BK : kb);
+      if (!SPLIT && refill) {
+        ca.issue(nx.a, dst, wave, p.lda, p.M, nx.k, nx.kend);
+        cb.issue(nx.b, dst + A_BYTES, wave, p.ldb, p.N, nx.k, nx.kend);
+      }
       load_unit<BM, BN, AK, BKC, TN, NKS, BK>(af, bfr, st, st + A_BYTES, fa, fb, u);
+      if (SPLIT && refill) ca.issue(nx.a, dst, wave, p.lda, p.M, nx.k, nx.kend);
       if constexpr (CS) {
         if (u == 0 && cs_on && t == cs_next) {
           cs.tile(st + A_BYTES);
@@ -787,11 +859,12 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
         }
       }
       __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the unit's fragments are in registers
-      if (grp == 1 && u == U - 1) wait_next(t);
+      if (grp == 1 && u == U - 1) wait_next(t, SPLIT && U == 1);
       phase_barrier();
       // compute phase
+      if (SPLIT && refill) cb.issue(nx.b, dst + A_BYTES, wave, p.ldb, p.N, nx.k, nx.kend);
       mma_unit<TN>(acc, af, bfr);
-      if (grp == 0 && u == U - 1) wait_next(t);
+      if (grp == 0 && u == U - 1) wait_next(t, false);
       phase_barrier();
     }
     sc = sc + 1 == NST ? 0 : sc + 1;
