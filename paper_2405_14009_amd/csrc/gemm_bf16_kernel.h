@@ -211,13 +211,34 @@ __device__ __forceinline__ bf16x8 frag(const char* tile, const FragOffsets<ROWS,
 // k-step's share of LDS reads) so the reads stay ahead of their use.
 // step(ks) runs at the head of k-step ks, after the fragment reads issued
 // before it (the kernels issue their next k-tile's copies from it).
+// DEFER: the MFMAs of the last k-step are left for the next call, which
+// issues them from (pa, pb) right behind its first fragment reads, so the
+// matrix core has work while those reads are in flight after the k-tile
+// barrier; mma_flush adds the last pending product.  (Zero fragments make the
+// first call's pending MFMAs a no-op.)
 struct NoStep {
   __device__ __forceinline__ void operator()(int) const {}
 };
-template <int BM, int BN, bool AK, bool BKC, int TN, int NKS, int BK, typename Step = NoStep>
+template <int TN>
+__device__ __forceinline__ void mma_flush(f32x16 (&acc)[4][TN], const bf16x8 (&pa)[4], const bf16x8 (&pb)[TN]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa[i], pb[j], acc[i][j], 0, 0, 0);
+}
+template <int TN>
+__device__ __forceinline__ void mma_pending_clear(bf16x8 (&pa)[4], bf16x8 (&pb)[TN]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) pa[i] = bf16x8{};
+#pragma unroll
+  for (int j = 0; j < TN; ++j) pb[j] = bf16x8{};
+}
+template <int BM, int BN, bool AK, bool BKC, int TN, int NKS, int BK, bool DEFER, typename Step>
 __device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][TN], const char* ta, const char* tb,
                                          const FragOffsets<BM, AK, 4, NKS, BK>& fa,
-                                         const FragOffsets<BN, BKC, TN, NKS, BK>& fb, Step step = Step()) {
+                                         const FragOffsets<BN, BKC, TN, NKS, BK>& fb, Step step,
+                                         bf16x8 (&pa)[4], bf16x8 (&pb)[TN]) {
   constexpr int READS = 4 * (AK ? 1 : 2) + TN * (BKC ? 1 : 2);  // LDS read instructions per k-step
   constexpr int NMFMA = 4 * TN;
   constexpr int PER = (READS + NMFMA - 1) / NMFMA;
@@ -227,6 +248,10 @@ __device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][TN], const char* ta, c
 #pragma unroll
   for (int j = 0; j < TN; ++j) bfr[0][j] = frag(tb, fb, j, 0);
   __builtin_amdgcn_sched_group_barrier(0x100, READS, 0);
+  if constexpr (DEFER) {
+    mma_flush<TN>(acc, pa, pb);
+    __builtin_amdgcn_sched_group_barrier(0x008, NMFMA, 0);
+  }
 #pragma unroll
   for (int ks = 0; ks < NKS; ++ks) {
     const int c = ks & 1;
@@ -238,6 +263,13 @@ __device__ __forceinline__ void mma_tile(f32x16 (&acc)[4][TN], const char* ta, c
       for (int i = 0; i < 4; ++i) af[c ^ 1][i] = frag(ta, fa, i, ks + 1);
 #pragma unroll
       for (int j = 0; j < TN; ++j) bfr[c ^ 1][j] = frag(tb, fb, j, ks + 1);
+    }
+    if (DEFER && ks + 1 == NKS) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pa[i] = af[c][i];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) pb[j] = bfr[c][j];
+      break;
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -460,7 +492,12 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
   // the A slices at the head of the first k-step, the B slices at the head of
   // the second (one burst of all of them ahead of the first MFMAs held those
   // MFMAs back: 5-11 % longer products).
+  // The weight-gradient layout defers each k-tile's last MFMAs (mma_tile):
+  // 1-4 % shorter products there; the other layouts measured slower with it.
   static_assert(NKS >= 2, "the refill spans two k-steps");
+  constexpr bool DEFER = !AK && !BKC;
+  bf16x8 pa[4], pb[TN];
+  mma_pending_clear<TN>(pa, pb);
 #pragma unroll
   for (int i = 0; i < NST - 1; ++i)
     if (i < nk) issue(lds + i * STAGE, kb + i * BK);
@@ -475,10 +512,10 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
     const Src nx = source(refill ? kb + (t + NST - 1) * BK : kb);
     char* dst = lds + si * STAGE;
     const char* st = lds + sc * STAGE;
-    mma_tile<BM, BN, AK, BKC, TN, NKS, BK>(acc, st, st + A_BYTES, fa, fb, [&](int ks) {
+    mma_tile<BM, BN, AK, BKC, TN, NKS, BK, DEFER>(acc, st, st + A_BYTES, fa, fb, [&](int ks) {
       if (refill && ks == 0) ca.issue(nx.a, dst, wave, p.lda, p.M, nx.k, nx.kend);
       if (refill && ks == 1) cb.issue(nx.b, dst + A_BYTES, wave, p.ldb, p.N, nx.k, nx.kend);
-    });
+    }, pa, pb);
     if constexpr (CS) {
       // while the tile's MFMAs drain; the stage stays valid until the next barrier
       __builtin_amdgcn_sched_barrier(0);
@@ -491,6 +528,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
     si = si + 1 == NST ? 0 : si + 1;
   }
 
+  if constexpr (DEFER) mma_flush<TN>(acc, pa, pb);
   // LDS is free once every wave is past its last k-tile.
   __builtin_amdgcn_sched_barrier(0);
   __syncthreads();
@@ -510,9 +548,10 @@ __global__ __launch_bounds__(64 * NW) void gemm_bf16_kernel(GemmParams p) {
 // are the ones that share operand panels in its L2.  Between two tiles the
 // next tile's first k-tile is copied into stage 0 before the finished tile's
 // epilogue runs, and the epilogue stages its rows through LDS above stage 0,
-// so that copy is in flight while the epilogue computes and stores.
+// so that copy is in flight while the epilogue computes and stores.  DEFER:
+// each k-tile's last MFMAs are deferred as mma_tile describes.
 // Requirements (checked by the launcher): batch * heads == 1, ntiles % 8 == 0.
-template <int EPI, bool AK, bool BKC>
+template <int EPI, bool AK, bool BKC, bool DEFER>
 __global__ __launch_bounds__(512) void gemm_bf16_persist_kernel(GemmParams p) {
   constexpr int BM = 256, BN = 256, NW = 8, BK = 64, NST = 2;
   constexpr int WN_ = 4, TN = 2, NKS = 4;
@@ -596,6 +635,8 @@ __global__ __launch_bounds__(512) void gemm_bf16_persist_kernel(GemmParams p) {
     ColSums<BN, BK> cs;
     if (cs_on) cs.init(threadIdx.x);
     int sc = 0, si = 1;
+    bf16x8 pa[4], pb[TN];  // the deferred last k-step of each k-tile (mma_tile)
+    mma_pending_clear<TN>(pa, pb);
     for (int t = 0; t < nk; ++t) {
       __builtin_amdgcn_sched_barrier(0);
       wait_vmcnt<0>();
@@ -606,10 +647,10 @@ __global__ __launch_bounds__(512) void gemm_bf16_persist_kernel(GemmParams p) {
       const Src nx = source(refill ? (t + 1) * BK : 0);
       char* dst = lds + si * STAGE;
       const char* st = lds + sc * STAGE;
-      mma_tile<BM, BN, AK, BKC, TN, NKS, BK>(acc, st, st + A_BYTES, fa, fb, [&](int ks) {
+      mma_tile<BM, BN, AK, BKC, TN, NKS, BK, DEFER>(acc, st, st + A_BYTES, fa, fb, [&](int ks) {
         if (refill && ks == 0) ca.issue(nx.a, dst, wave, p.lda, p.M, nx.k, nx.kend);
         if (refill && ks == 1) cb.issue(nx.b, dst + A_BYTES, wave, p.ldb, p.N, nx.k, nx.kend);
-      });
+      }, pa, pb);
       if constexpr (CS) {
         __builtin_amdgcn_sched_barrier(0);
         if (cs_on && t == cs_next) {
@@ -620,6 +661,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persist_kernel(GemmParams p) {
       sc ^= 1;
       si ^= 1;
     }
+    if constexpr (DEFER) mma_flush<TN>(acc, pa, pb);
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();  // every wave is past the last k-tile: both stages are free
     const int cm0 = m0, cn0 = n0, ctm = tm;
@@ -879,16 +921,19 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
     if (cs_on) cs.finish((float*)lds, p, tm, n0, threadIdx.x);
   }
   // The partner's slot is read only by this wave, so after the reduction it
-  // serves as this wave's epilogue tile.
+  // serves as this wave's epilogue tile.  (The gradient-accumulating
+  // epilogue fetches each block-row's inputs as it reaches it: fetched a
+  // block-row ahead they spill registers next to the k-split state.)
+  constexpr bool LOOK = EPI != EPI_F32_ACC;
   float* mine = (float*)(lds + wave * SLOT);
   float* theirs = (float*)(lds + ((1 - kg) * NWS + ws) * SLOT);
   static_assert(EPI_BYTES <= SLOT, "epilogue tile fits a reduction slot");
   if (kg == 0) {
     ksplit_reduce<TN, 0>(acc, mine, theirs, lane);
-    epilogue<EPI, TN, 0, 2>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
+    epilogue<EPI, TN, 0, 2, LOOK>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
   } else {
     ksplit_reduce<TN, 1>(acc, mine, theirs, lane);
-    epilogue<EPI, TN, 2, 4>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
+    epilogue<EPI, TN, 2, 4, LOOK>(p, acc, theirs, m0 + wm * 128, n0 + wn * (BN / WN_), lane, c_off);
   }
 }
 
@@ -916,7 +961,13 @@ hipError_t launch_bf16_persist(const GemmParams& p, hipStream_t s) {
   const int ntiles = ((p.M + 255) / 256) * ((p.N + 255) / 256);
   const int per_xcd = std::max(1, device_compute_units() / 8);
   const int nq = std::min(ntiles / 8, per_xcd);
-  hipLaunchKernelGGL((gemm_bf16_persist_kernel<EPI, AK, BKC>), dim3(8 * nq), dim3(512), 0, s, p);
+  // Deferred last k-steps (mma_tile) pay off on the long reductions of
+  // batched weight gradients (-2 % batched, -7 % for one-round launches), not
+  // on single micro-batch ones (+2.4 % at K = 2048).
+  if (p.K >= 8192)
+    hipLaunchKernelGGL((gemm_bf16_persist_kernel<EPI, AK, BKC, true>), dim3(8 * nq), dim3(512), 0, s, p);
+  else
+    hipLaunchKernelGGL((gemm_bf16_persist_kernel<EPI, AK, BKC, false>), dim3(8 * nq), dim3(512), 0, s, p);
   return hipGetLastError();
 }
 

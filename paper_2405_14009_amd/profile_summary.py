@@ -62,8 +62,8 @@ def sources_digest() -> str:
 def kernel_class(name: str) -> str:
     # the one-tile and ping-pong bf16 GEMM kernels end their template arguments
     # with (A k-contiguous, B k-contiguous, epilogue); the persistent kernel
-    # has them as (epilogue, A k-contiguous, B k-contiguous)
-    m = re.search(r"gemm_bf16_persist_kernel<(\d+),\s*(true|false),\s*(true|false)>", name)
+    # begins with (epilogue, A k-contiguous, B k-contiguous)
+    m = re.search(r"gemm_bf16_persist_kernel<(\d+),\s*(true|false),\s*(true|false)(?:,\s*(?:true|false))?>", name)
     if m:
         epi, ak, bk = int(m.group(1)), m.group(2), m.group(3)
     else:
