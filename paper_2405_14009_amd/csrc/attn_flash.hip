@@ -296,6 +296,33 @@ struct FwdState {
   }
 };
 
+// Key masking of a score block whose lane column is a query (lane l: query
+// qq = q0 + l % 32).  Element r of 32-key half j holds key
+//   k0 + 32 j + 4 (l / 32) + kofs(r),  kofs(r) = 8 (r / 4) + r % 4,
+// which is masked when it lies past the sequence end or, causal, after qq,
+// i.e. when 32 j + kofs(r) > key_room = min(qq (causal), s - 1) - k0 - 4 (l / 32):
+// one compare per element against a constant.  Callers take this path only
+// for the blocks that straddle the diagonal or the sequence end.
+__device__ __forceinline__ constexpr int kofs(int r) { return 8 * (r >> 2) + (r & 3); }
+template <bool CAUSAL>
+__device__ __forceinline__ int key_room(int k0, int qq, int lane, const AttnArgs& p) {
+  const int last = CAUSAL ? min(qq, p.s - 1) : p.s - 1;
+  return last - k0 - 4 * (lane >> 5);
+}
+// A wave-uniform condition as such for the compiler (its operands are
+// uniform, but the compiler cannot always tell): the masking then stays a
+// branch that only the blocks needing it take, instead of selects that
+// every block executes.
+__device__ __forceinline__ bool uniform(bool c) { return __builtin_amdgcn_readfirstlane((int)c) != 0; }
+template <int NJ>
+__device__ __forceinline__ void mask_scores(f32x16 (&sc)[NJ], int room, float v) {
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (32 * j + kofs(r) > room) sc[j][r] = v;
+}
+
 // One key block (keys k0..k0+63; K tile kt, V tile vt) for the wave's queries
 // q0..q0+31 (this lane's query qq).
 template <bool CAUSAL>
@@ -307,20 +334,16 @@ __device__ __forceinline__ void fwd_block(FwdState& st, const bf16x8 (&qf)[HD / 
   zero(sc[0]);
   zero(sc[1]);
   two_chains<2>(sc[0], kt, 0, qf, sc[1], kt, 1, qf, ro);
-  const bool need_mask = (CAUSAL && k0 + 63 > q0) || (k0 + 64 > p.s);
-  // Row maximum over the raw scores (the scale is positive), masked keys at
-  // -inf; the scale is folded into the exponent's FMA below.
+  // Masked keys (past the sequence end or, causal, after the query) at -inf.
+  if (uniform((CAUSAL && k0 + 63 > q0) || k0 + 64 > p.s))
+    mask_scores<2>(sc, key_room<CAUSAL>(k0, qq, lane, p), -INFINITY);
+  // Row maximum over the raw scores (the scale is positive); the scale is
+  // folded into the exponent's FMA below.
   float mx = -INFINITY;
 #pragma unroll
   for (int j = 0; j < 2; ++j)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      if (need_mask) {
-        const int key = k0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (key >= p.s || (CAUSAL && key > qq)) sc[j][r] = -INFINITY;
-      }
-      mx = fmaxf(mx, sc[j][r]);
-    }
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[j][r]);
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.sl2;
   // Lazy rescaling: the reference maximum moves only when a row's maximum
   // exceeds it by more than 8 (base 2), so most key blocks skip rescaling O
@@ -623,7 +646,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_k(AttnArgs p) {
     const char* ot = st + TILE64;
     const float* lse = (const float*)(st + 2 * TILE64);
     const float* dvv = (const float*)(st + 2 * TILE64 + 1024);
-    const bool need_mask = CAUSAL && qs < k0w + 31;
+    const bool need_mask = uniform(CAUSAL && qs < k0w + 31);
     // the two 32-query halves of the block in turn (one half's scores live)
 #pragma unroll 1
     for (int j = 0; j < 2; ++j) {
@@ -631,21 +654,30 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_k(AttnArgs p) {
       zero(sc);
       zero(dp);
       two_chains<2>(sc, qt, j, kf, dp, ot, j, vf, ro);
+      float Dv[16];
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
         const int ql = 32 * j + 8 * rg + 4 * (lane >> 5);
         const float4 L4 = *(const float4*)(lse + ql);
         const float4 D4 = *(const float4*)(dvv + ql);
-        const float Lv[4] = {L4.x, L4.y, L4.z, L4.w}, Dv[4] = {D4.x, D4.y, D4.z, D4.w};
+        const float Lv[4] = {L4.x, L4.y, L4.z, L4.w};
+        Dv[4 * rg] = D4.x;
+        Dv[4 * rg + 1] = D4.y;
+        Dv[4 * rg + 2] = D4.z;
+        Dv[4 * rg + 3] = D4.w;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = 4 * rg + e;
-          float pv = __builtin_amdgcn_exp2f(sc[r] * p.sl2 - Lv[e]);
-          if (need_mask && key > qs + ql + e) pv = 0.f;
-          sc[r] = pv;
-          dp[r] = pv * (dp[r] - Dv[e]);
-        }
+        for (int e = 0; e < 4; ++e) sc[4 * rg + e] = __builtin_amdgcn_exp2f(sc[4 * rg + e] * p.sl2 - Lv[e]);
       }
+      // element r holds query qs + 32 j + 4 (l / 32) + kofs(r): masked when
+      // that query precedes this lane's key
+      if (need_mask) {
+        const int room = key - qs - 32 * j - 4 * (lane >> 5);
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (kofs(r) < room) sc[r] = 0.f;
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dp[r] = sc[r] * (dp[r] - Dv[r]);
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
         const int t = 2 * j + hf;
@@ -721,24 +753,21 @@ __device__ __forceinline__ void bwdq_block(f32x16 (&dq)[HD / 32], const BwdQRows
                                            const char* vt, const RowOffs& ro, const TrOffs& to, int k0,
                                            int q0, int qq, int lane, const AttnArgs& p) {
   if (CAUSAL && k0 > q0 + 31) return;
-  const bool need_mask = (CAUSAL && k0 + 63 > q0) || (k0 + 64 > p.s);
+  const bool need_mask = uniform((CAUSAL && k0 + 63 > q0) || (k0 + 64 > p.s));
+  const int room = key_room<CAUSAL>(k0, qq, lane, p);
   // the two 32-key halves of the block in turn (one half's scores live)
 #pragma unroll 1
   for (int j = 0; j < 2; ++j) {
     if (CAUSAL && k0 + 32 * j > q0 + 31) break;  // this half is after every query of the wave
-    f32x16 sc, dp;
-    zero(sc);
+    f32x16 sc[1], dp;
+    zero(sc[0]);
     zero(dp);
-    two_chains<2>(sc, kt, j, w.qf, dp, vt, j, w.of, ro);
+    two_chains<2>(sc[0], kt, j, w.qf, dp, vt, j, w.of, ro);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      float pv = __builtin_amdgcn_exp2f(sc[r] * p.sl2 - w.Lq);
-      if (need_mask) {
-        const int key = k0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (key >= p.s || (CAUSAL && key > qq)) pv = 0.f;
-      }
-      dp[r] = pv * (dp[r] - w.Dq);
-    }
+    for (int r = 0; r < 16; ++r) sc[0][r] = __builtin_amdgcn_exp2f(sc[0][r] * p.sl2 - w.Lq);
+    if (need_mask) mask_scores<1>(sc, room - 32 * j, 0.f);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dp[r] = sc[0][r] * (dp[r] - w.Dq);
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
       const bf16x8 sf = pack_half(dp, hf);
