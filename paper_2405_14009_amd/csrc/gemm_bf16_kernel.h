@@ -741,9 +741,9 @@ __device__ __forceinline__ void phase_barrier() {
 // wave tiles and multiplies k-steps 2 g, 2 g + 1 of every k-tile (one unit);
 // the two groups' partial sums are added through LDS at the end.  (The unit
 // loop also allows several units per k-tile, as a single k-group would need.)
-// Copies.  Tile t + NST - 1 is issued in tile t's first unit: in its memory
-// phase ahead of the fragment reads, or, with k-contiguous B tiles, the A
-// slices after the reads and the B slices at the head of the compute phase.
+// Copies.  Tile t + NST - 1 is issued in tile t's first unit: its A slices
+// after the memory phase's fragment reads, its B slices ahead of them or,
+// with k-contiguous B tiles, at the head of the compute phase.
 // Tile t + 1 is first read in group 0's first memory phase of tile t + 1;
 // before the barrier that opens that phase each wave waits for its own share
 // (group 0 after its last compute phase of tile t, group 1 after its last
@@ -855,10 +855,10 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
     ca.issue(sr.a, st, wave, p.lda, p.M, sr.k, sr.kend);
     cb.issue(sr.b, st + A_BYTES, wave, p.ldb, p.N, sr.k, sr.kend);
   };
-  // With k-contiguous B tiles (the input-gradient products) the refill's A
-  // slices follow the unit's fragment reads and its B slices open the compute
-  // phase (6-8 % shorter products than one burst ahead of the reads; with
-  // m/n-contiguous B tiles the split measured no faster).
+  // The refill's A slices follow the unit's fragment reads.  Its B slices open
+  // the compute phase when the B tiles are k-contiguous (the input-gradient
+  // products) and precede the fragment reads otherwise (the forward products):
+  // 6-8 % and 2-4 % shorter products than one burst of both ahead of the reads.
   constexpr bool SPLIT = BKC;
   // Waits until this wave's share of tile t + 1 has landed (the copies of
   // tiles t + 2 .. t + NST - 1 issued so far may stay in flight: all of them,
@@ -888,12 +888,9 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
       const bool refill = u == 0 && t + NST - 1 < nk;
       char* dst = lds + si * STAGE;
       const Src nx = source(refill ? kb + (t + NST - 1) * BK : kb);
-      if (!SPLIT && refill) {
-        ca.issue(nx.a, dst, wave, p.lda, p.M, nx.k, nx.kend);
-        cb.issue(nx.b, dst + A_BYTES, wave, p.ldb, p.N, nx.k, nx.kend);
-      }
+      if (!SPLIT && refill) cb.issue(nx.b, dst + A_BYTES, wave, p.ldb, p.N, nx.k, nx.kend);
       load_unit<BM, BN, AK, BKC, TN, NKS, BK>(af, bfr, st, st + A_BYTES, fa, fb, u);
-      if (SPLIT && refill) ca.issue(nx.a, dst, wave, p.lda, p.M, nx.k, nx.kend);
+      if (refill) ca.issue(nx.a, dst, wave, p.lda, p.M, nx.k, nx.kend);
       if constexpr (CS) {
         if (u == 0 && cs_on && t == cs_next) {
           cs.tile(st + A_BYTES);
