@@ -707,16 +707,24 @@ __device__ __forceinline__ void load_unit(bf16x8 (&af)[2][4], bf16x8 (&bfr)[2][T
   }
 }
 
-template <int TN>
+// The unit's 4 x TN x 2 MFMAs from registers; with MID, mid() runs between
+// its two k-steps.
+template <int TN, bool MID, typename Mid>
 __device__ __forceinline__ void mma_unit(f32x16 (&acc)[4][TN], const bf16x8 (&af)[2][4],
-                                         const bf16x8 (&bfr)[2][TN]) {
+                                         const bf16x8 (&bfr)[2][TN], Mid mid) {
 #pragma unroll
-  for (int s = 0; s < 2; ++s)
+  for (int s = 0; s < 2; ++s) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s][i], bfr[s][j], acc[i][j], 0, 0, 0);
+    if (MID && s == 0) {
+      __builtin_amdgcn_sched_barrier(0);
+      mid();
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
 }
 
 // Workgroup-wide barrier that the compiler may not move any instruction across.
@@ -729,10 +737,11 @@ __device__ __forceinline__ void phase_barrier() {
 // Ping-pong schedule.  Waves w and w + 4 share a SIMD (waves are dealt to the
 // four SIMDs in turn); the two groups {0..3} and {4..7} run the same
 // sequence of alternating phases, one phase apart:
-//   memory phase:  issue this wave's share of a k-tile copy (first unit of a
-//                  tile only), read one unit's fragments (two k-steps) from
-//                  LDS into registers and wait for them;
-//   compute phase: the unit's 4 x TN x 2 MFMAs from registers, no LDS access.
+//   memory phase:  read one unit's fragments (two k-steps) from LDS into
+//                  registers and wait for them;
+//   compute phase: the unit's 4 x TN x 2 MFMAs from registers, no LDS reads.
+// The first unit of a tile also issues this wave's share of a k-tile copy,
+// spread over both phases (Copies, below).
 // Every phase ends at a workgroup barrier, so while one group multiplies the
 // other reads, and each SIMD always has one wave with MFMAs to issue: the
 // matrix core no longer idles while both waves of a SIMD sit at the same
@@ -743,7 +752,7 @@ __device__ __forceinline__ void phase_barrier() {
 // loop also allows several units per k-tile, as a single k-group would need.)
 // Copies.  Tile t + NST - 1 is issued in tile t's first unit: its A slices
 // after the memory phase's fragment reads, its B slices ahead of them or,
-// with k-contiguous B tiles, at the head of the compute phase.
+// with k-contiguous B tiles, between the compute phase's two k-steps.
 // Tile t + 1 is first read in group 0's first memory phase of tile t + 1;
 // before the barrier that opens that phase each wave waits for its own share
 // (group 0 after its last compute phase of tile t, group 1 after its last
@@ -855,10 +864,11 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
     ca.issue(sr.a, st, wave, p.lda, p.M, sr.k, sr.kend);
     cb.issue(sr.b, st + A_BYTES, wave, p.ldb, p.N, sr.k, sr.kend);
   };
-  // The refill's A slices follow the unit's fragment reads.  Its B slices open
-  // the compute phase when the B tiles are k-contiguous (the input-gradient
-  // products) and precede the fragment reads otherwise (the forward products):
-  // 6-8 % and 2-4 % shorter products than one burst of both ahead of the reads.
+  // The refill's A slices follow the unit's fragment reads.  Its B slices go
+  // out between the compute phase's two k-steps when the B tiles are
+  // k-contiguous (the input-gradient products) and ahead of the fragment reads
+  // otherwise (the forward products): 8-12 % and 2-4 % shorter products than
+  // one burst of both ahead of the reads.
   constexpr bool SPLIT = BKC;
   // Waits until this wave's share of tile t + 1 has landed (the copies of
   // tiles t + 2 .. t + NST - 1 issued so far may stay in flight: all of them,
@@ -901,8 +911,9 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmParams p) {
       if (grp == 1 && u == U - 1) wait_next(t, SPLIT && U == 1);
       phase_barrier();
       // compute phase
-      if (SPLIT && refill) cb.issue(nx.b, dst + A_BYTES, wave, p.ldb, p.N, nx.k, nx.kend);
-      mma_unit<TN>(acc, af, bfr);
+      mma_unit<TN, SPLIT>(acc, af, bfr, [&]() {
+        if (refill) cb.issue(nx.b, dst + A_BYTES, wave, p.ldb, p.N, nx.k, nx.kend);
+      });
       if (grp == 0 && u == U - 1) wait_next(t, false);
       phase_barrier();
     }
