@@ -28,6 +28,18 @@ __device__ __forceinline__ float adam_one(float p, float g, float& m, float& v, 
   return p - adam_update(m, v, eps, step_size, inv_sqrt_bc2);
 }
 
+// The fp32 streams are read and written once per step: non-temporal accesses
+// keep them from displacing cached data (-1.6 % AdamW time).
+typedef float vf4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 ld_nt(const float4* q) {
+  const vf4 t = __builtin_nontemporal_load((const vf4*)q);
+  return make_float4(t.x, t.y, t.z, t.w);
+}
+__device__ __forceinline__ void st_nt(float4* q, float4 v) {
+  const vf4 t = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(t, (vf4*)q);
+}
+
 // bf16 working copy of 4 consecutive weights: one 8-byte store.
 __device__ __forceinline__ void store_bf16x4(bf16* o, float4 w) {
   const bf16 t[4] = {(bf16)w.x, (bf16)w.y, (bf16)w.z, (bf16)w.w};
@@ -41,15 +53,15 @@ __global__ __launch_bounds__(NT) void adamw_k(float4* __restrict__ p, const floa
                                               float b1, float b2, float eps, float wd,
                                               float step_size, float inv_sqrt_bc2, float gs) {
   for (long i = blockIdx.x * (long)NT + threadIdx.x; i < n4; i += (long)gridDim.x * NT) {
-    float4 pp = p[i], gg = g[i], mm = m[i], vv = v[i];
+    float4 pp = ld_nt(p + i), gg = ld_nt(g + i), mm = ld_nt(m + i), vv = ld_nt(v + i);
     const bool dec = i < nd4;
     pp.x = adam_one(pp.x, gg.x, mm.x, vv.x, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
     pp.y = adam_one(pp.y, gg.y, mm.y, vv.y, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
     pp.z = adam_one(pp.z, gg.z, mm.z, vv.z, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
     pp.w = adam_one(pp.w, gg.w, mm.w, vv.w, dec, lr, b1, b2, eps, wd, step_size, inv_sqrt_bc2, gs);
-    p[i] = pp;
-    m[i] = mm;
-    v[i] = vv;
+    st_nt(p + i, pp);
+    st_nt(m + i, mm);
+    st_nt(v + i, vv);
     if (wb != nullptr && dec) store_bf16x4(wb + 4 * i, pp);
   }
 }
