@@ -30,15 +30,18 @@
 //     row/column, the same operand layout as the k-contiguous case.
 //
 // What bounds these kernels on MI355X (counters, and variants with one
-// component switched off): the copies.  Each CU keeps about 64 L2 read
-// requests of 128 bytes in flight, so at the observed 300-450 cycles of
-// average latency it receives 18-27 bytes per clock, while a 256 x 256 x 64
-// k-tile (64 KB) feeds 2048 MFMA cycles per SIMD.  Without the copies the same
-// kernels reach 1.5-1.9 PFLOP/s; without the fragment reads they barely
-// change.  Deeper rings (four or five stages of 32), register staging
-// (buffer_load + ds_write), padded leading dimensions and a one-wave-per-SIMD
-// layout did not help; the ping-pong schedule and a tile order whose 32
-// concurrent tiles per XCD share fewer operand panels did (256 x 128 tiles).
+// component switched off): the copies.  A CU keeps 60-85 L2 read requests of
+// 128 bytes in flight at 350-450 cycles of average latency, so it receives
+// 20-25 bytes per clock, while a 256 x 256 x 64 k-tile (64 KB) feeds 2048 MFMA
+// cycles per SIMD (32 bytes per clock at the full rate); the units that return
+// the copied lines to LDS are busy about 70 % of the time.  Without the copies
+// the same kernels reach 1.5-1.9 PFLOP/s; without the fragment reads they
+// barely change.  Where in the multiply of a k-tile the next refill is issued
+// matters (5-12 %, see the kernels); deeper rings of 32-deep k-tiles, register
+// staging (buffer_load + ds_write), padded leading dimensions and a
+// one-wave-per-SIMD layout did not help; the ping-pong schedule and a tile
+// order whose 32 concurrent tiles per XCD share fewer operand panels did
+// (256 x 128 tiles).
 #pragma once
 
 #include <algorithm>

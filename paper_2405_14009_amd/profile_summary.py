@@ -47,15 +47,26 @@ from collections import defaultdict
 COPY_BYTES = 1 << 30  # per copy dispatch of bench.py --copy-probe (read and write)
 
 
-def sources_digest() -> str:
-    """sha256 over the kernel and runtime sources (name + content, sorted)."""
-    d = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
+_COMMENT = re.compile(r"//[^\n]*|/\*.*?\*/", re.S)
+
+
+def code_text(src: str) -> str:
+    """Source text without comments, trailing blanks and empty lines: what
+    the compiler sees, so that editing a comment keeps the digest."""
+    lines = (line.rstrip() for line in _COMMENT.sub("", src).splitlines())
+    return "\n".join(line for line in lines if line)
+
+
+def sources_digest(d: str = None) -> str:
+    """sha256 over the code of the kernel and runtime sources (name + code
+    text, sorted by name)."""
+    d = d or os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
     h = hashlib.sha256()
     for name in sorted(os.listdir(d)):
         if name.endswith((".hip", ".h", ".cpp")):
             h.update(name.encode())
-            with open(os.path.join(d, name), "rb") as f:
-                h.update(f.read())
+            with open(os.path.join(d, name), encoding="utf-8") as f:
+                h.update(code_text(f.read()).encode())
     return h.hexdigest()
 
 

@@ -1,6 +1,7 @@
 """Host logic of the rocprofv3 summary (paper_2405_14009_amd/profile_summary.py):
-kernel classes of the library's kernel names, and the arithmetic of the MFMA
-and L1 -> L2 counter passes on small synthetic counter files."""
+kernel classes of the library's kernel names, the arithmetic of the MFMA and
+L1 -> L2 counter passes on small synthetic counter files, and the source
+digest that ties a summary to the kernel code it was taken with."""
 import csv
 
 import pytest
@@ -88,3 +89,13 @@ def test_l2_pass_arithmetic(tmp_path):
 def test_sources_digest_is_stable():
     assert ps.sources_digest() == ps.sources_digest()
     assert len(ps.sources_digest()) == 64
+
+
+def test_sources_digest_ignores_comments_only(tmp_path):
+    src = tmp_path / "k.hip"
+    src.write_text("// header\n__global__ void k(int* p) {\n  p[0] = 1;  // store\n}\n")
+    base = ps.sources_digest(str(tmp_path))
+    src.write_text("// a new header\n/* and a block\n comment */\n__global__ void k(int* p) {\n  p[0] = 1;\n}\n")
+    assert ps.sources_digest(str(tmp_path)) == base
+    src.write_text("// header\n__global__ void k(int* p) {\n  p[0] = 2;  // store\n}\n")
+    assert ps.sources_digest(str(tmp_path)) != base
