@@ -38,8 +38,9 @@
 // the same kernels reach 1.5-1.9 PFLOP/s; without the fragment reads they
 // barely change.  Where in the multiply of a k-tile the next refill is issued
 // matters (5-12 %, see the kernels); deeper rings of 32-deep k-tiles, register
-// staging (buffer_load + ds_write), padded leading dimensions and a
-// one-wave-per-SIMD layout did not help; the ping-pong schedule and a tile
+// staging (buffer_load + ds_write, also two k-tiles ahead), an L2 prefetch of
+// the k-tile after next, padded leading dimensions and a one-wave-per-SIMD
+// layout did not help; the ping-pong schedule and a tile
 // order whose 32 concurrent tiles per XCD share fewer operand panels did
 // (256 x 128 tiles).
 #pragma once
