@@ -93,14 +93,8 @@ struct Copier {
   }
   __device__ __forceinline__ void issue(const i32x4& r, char* tile, int wave, long ld, int MN, int k0,
                                         int K) const {
-    issue_part<0, NI>(r, tile, wave, ld, MN, k0, K);
-  }
-  // slices Q0 .. Q1-1 of this wave's share
-  template <int Q0, int Q1>
-  __device__ __forceinline__ void issue_part(const i32x4& r, char* tile, int wave, long ld, int MN, int k0,
-                                             int K) const {
 #pragma unroll
-    for (int q = Q0; q < Q1; ++q) {
+    for (int q = 0; q < NI; ++q) {
       uint32_t off;
       if (KC) {
         const int k = k0 + kk;
@@ -220,9 +214,6 @@ __device__ __forceinline__ bf16x8 frag(const char* tile, const FragOffsets<ROWS,
 // matrix core has work while those reads are in flight after the k-tile
 // barrier; mma_flush adds the last pending product.  (Zero fragments make the
 // first call's pending MFMAs a no-op.)
-struct NoStep {
-  __device__ __forceinline__ void operator()(int) const {}
-};
 template <int TN>
 __device__ __forceinline__ void mma_flush(f32x16 (&acc)[4][TN], const bf16x8 (&pa)[4], const bf16x8 (&pb)[TN]) {
 #pragma unroll
